@@ -1,0 +1,254 @@
+#!/usr/bin/env python3
+"""Benchmark of the WeDLM streaming parallel-decode step on one MI355X.
+
+A step is one pass of the whole hot path over one batch: wedlm_reorder,
+wedlm_window_attn, wedlm_score and wedlm_commit, on synthetic inputs that
+are already resident in HBM.  The window state (win_tok, win_start) is reset
+from a pristine device copy before every step, so every timed step does the
+configured workload's work (the reset copies are inside the timed region).
+Small workloads rotate over several input sets so that no timed step finds
+its inputs in the 256 MB last-level cache.
+
+Prints ONE JSON line: window tokens/s (B*W per step time), the roofline of
+the dominant kernel (window attention: algorithmic bytes per launch over its
+HIP-event-timed average duration, against 8 TB/s), and the fp64 CPU oracle
+timed on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("decode-step window tokens/s (attn+score+commit); achieved HBM "
+          "GB/s % of peak")
+HBM_PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles",
+                            "window_attn_{wl}_traffic.txt")
+ATTN_SRC = os.path.join(ROOT, "paper_2512_22737_amd", "csrc",
+                        "window_attn.hip")
+
+
+def attn_bytes(wl, c):
+    """Algorithmic bytes of one wedlm_window_attn launch: the prefix K and V
+    (2 * 2 * D * Hkv bytes per cached position, read once), the window's
+    rotated Q/K/V read once, O (bf16) and lse (fp32) written once."""
+    kv = 4 * wl.D * wl.Hkv * int(sum(int(x) for x in c))
+    win = wl.B * wl.W * (wl.Hq + 2 * wl.Hkv) * wl.D * 2
+    out = wl.B * wl.W * wl.Hq * (wl.D * 2 + 4)
+    return kv + win + out
+
+
+def step_bytes(wl, c, n_masked, n_commit_rows):
+    """Algorithmic bytes of one step: reorder (qkv in, rotated q/k/v out),
+    attention, the masked rows' logits, KV append (read + write)."""
+    qkv = wl.B * wl.W * (wl.Hq + 2 * wl.Hkv) * wl.D * 2
+    return (2 * qkv + attn_bytes(wl, c) + 4 * wl.V * n_masked +
+            2 * 2 * 2 * wl.Hkv * wl.D * n_commit_rows)
+
+
+def read_traffic(wl_name):
+    """HBM traffic per attention launch from committed rocprofv3 counter
+    summaries, if they were taken on the current kernel source."""
+    path = TRAFFIC_FILE.format(wl=wl_name)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    src = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
+    if kv.get("source_sha256") != src:
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, d, seed):
+    """The fp64 oracle (as it stands) on sequence 0 of the same inputs:
+    reorder + RoPE, attention of all W rows x Hq heads over the full prefix,
+    entropy of the masked rows, commit.  BLAS limited to one thread."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    from oracle import wedlm_oracle as O
+    from paper_2512_22737_amd import workloads as WL
+    b = 0
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        win = list(map(int, d["win_tok"][b]))
+        c = int(d["win_start"][b])
+        perm, pos, _, n_obs = O.reorder(win, c)
+        q, k, v = O.rope_window(d["qkv_in"][b], perm, pos, wl.Hq, wl.Hkv,
+                                wl.theta)
+        kb, vb = WL.gather_prefix(d["k_cache"], d["v_cache"],
+                                  d["block_table"], b, c)
+        O.window_attn(q, k, v, O.bf16_to_f64(kb), O.bf16_to_f64(vb))
+        tok, H, _ = O.score(d["logits"][b], n_obs, wl.temp)
+        O.commit(win, c, O.to_f32_decision(H), tok, wl.tau, wl.lam,
+                 d["block_table"][b])
+        dt = time.perf_counter() - t0
+    return {"value": wl.W / dt, "unit": "window tokens/s", "cores": 1,
+            "kind": "oracle",
+            "sample": (f"sequence 0 of {wl.B} ({wl.W} window tokens, prefix "
+                       f"{c}): reorder+RoPE, attention of {wl.W} rows x "
+                       f"{wl.Hq} heads, entropy of {wl.W - n_obs} masked "
+                       f"rows over V={wl.V}, commit; {dt:.1f} s, fp64 numpy, "
+                       f"BLAS 1 thread; host has "
+                       f"{len(os.sched_getaffinity(0))} cores")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="long_prefix")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run a plain device copy of this size (for "
+                         "scaling HBM counters) and exit")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is "
+              "not supported (the multi-GPU sharding is a design note only)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2512_22737_amd import wedlm
+    from paper_2512_22737_amd import workloads as WL
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wedlm.lib()       # fails loudly when the HIP library is missing
+    dev = torch.device("cuda:0")
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "launches": 5}), flush=True)
+        return
+
+    wl = WL.WORKLOADS[args.workload]
+    if wl.steps > 1:
+        wl = wl.replace(steps=1)      # one step of the streaming shape
+    total_steps = args.warmup + args.steps
+    print(f"# generating inputs for {wl.name}", file=sys.stderr, flush=True)
+    d = WL.step_inputs(wl, seed=args.seed, nan_observed_rows=False)
+    c = d["win_start"]
+    n_masked = int((d["win_tok"] == -1).sum())
+    lead = d["win_tok"] != -1
+    n_commit_rows = int(sum(int(np.argmin(np.append(r, False)))
+                            for r in lead))
+    one_set = step_bytes(wl, c, n_masked, n_commit_rows)
+    n_sets = 1 if one_set >= (512 << 20) else min(
+        16, math.ceil((512 << 20) / one_set))
+
+    def up(a):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        if a.dtype == np.uint16:
+            t = t.view(torch.int16).view(torch.bfloat16)
+        return t.to(dev)
+
+    sets = []
+    for _ in range(n_sets):
+        sets.append({k: up(v) for k, v in d.items()
+                     if isinstance(v, np.ndarray)})
+    step = wedlm.DecodeStep(wl.B, wl.W, wl.Hq, wl.Hkv, wl.D, wl.V,
+                            int(c.max()), theta=wl.theta, tau=wl.tau,
+                            lam=wl.lam, temperature=wl.temp, device=dev)
+
+    def run(t, ev=None):
+        s = sets[t % n_sets]
+        s["win_tok"].copy_(s["win_tok_0"])
+        s["win_start"].copy_(s["win_start_0"])
+        step.reorder(s["win_tok"], s["win_start"], s["qkv_in"])
+        if ev is not None:
+            ev[0].record()
+        step.attn(s["k_cache"], s["v_cache"], s["block_table"],
+                  s["win_start"])
+        if ev is not None:
+            ev[1].record()
+        step.score(s["logits"])
+        step.commit(s["win_tok"], s["win_start"], s["k_cache"],
+                    s["v_cache"], s["block_table"])
+
+    for s in sets:
+        s["win_tok_0"] = s["win_tok"].clone()
+        s["win_start_0"] = s["win_start"].clone()
+
+    for t in range(args.warmup):
+        run(t)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True),
+            torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for t in range(args.steps):
+        run(args.warmup + t, evs[t])
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / args.steps
+    attn_ms = [a.elapsed_time(b) for a, b in evs]
+    attn_avg_s = sum(attn_ms) / len(attn_ms) / 1e3
+    status = int(step.status.abs().sum().item() +
+                 step.attn_status.abs().sum().item())
+    if status:
+        print(f"# warning: nonzero status words ({status})", file=sys.stderr)
+
+    a_bytes = attn_bytes(wl, c)
+    achieved = a_bytes / attn_avg_s / 1e9
+    s_bytes = step_bytes(wl, c, n_masked, n_commit_rows)
+    res = {
+        "metric": METRIC,
+        "value": wl.B * wl.W / (ms_step / 1e3),
+        "unit": "window tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "prefix": int(c.max()),
+                   "prefix_min": int(c.min()), "W": wl.W, "Hq": wl.Hq,
+                   "Hkv": wl.Hkv, "D": wl.D, "V": wl.V,
+                   "masked_rows": n_masked, "tau": wl.tau, "lambda": wl.lam,
+                   "temperature": wl.temp, "input_sets": n_sets},
+        "roofline": {"kernel": "wedlm_window_attn", "bound": "hbm",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": read_traffic(wl.name),
+                     "alg_bytes_per_launch": a_bytes,
+                     "avg_launch_us": attn_avg_s * 1e6},
+        "step_alg_bytes": s_bytes,
+        "step_hbm_gbps": s_bytes / (ms_step / 1e3) / 1e9,
+        "step_frac": s_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBPS,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("# timing the oracle on a sample", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(wl, d, args.seed)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -287,9 +287,11 @@ def rope_window(qkv_in_bits: np.ndarray, perm: Sequence[int],
                 pos: Sequence[int], Hq: int, Hkv: int, theta: float):
     """Gather one sequence's window rows into physical order and rotate Q
     and K at their logical positions.  qkv_in is [W, Hq+2Hkv, D] (bf16 bits,
-    logical order).  Returns q [W,Hq,D], k [W,Hkv,D], v [W,Hkv,D] fp64."""
+    logical order); perm/pos may list only the first physical rows.
+    Returns q [n,Hq,D], k [n,Hkv,D], v [n,Hkv,D] fp64, n = len(perm)."""
     x = bf16_to_f64(qkv_in_bits)
-    W, _, D = x.shape
+    D = x.shape[-1]
+    W = len(perm)
     q = np.empty((W, Hq, D))
     k = np.empty((W, Hkv, D))
     v = np.empty((W, Hkv, D))
@@ -311,7 +313,8 @@ def stream(win0: np.ndarray, c0: np.ndarray, steps: int,
            block_table: np.ndarray,
            prefix_kv: Optional[Callable[[int], tuple]] = None,
            attn_steps: Sequence[int] = (),
-           logits_row: Optional[Callable[[int, int, int], np.ndarray]] = None):
+           logits_row: Optional[Callable[[int, int, int], np.ndarray]] = None,
+           progress: Optional[Callable[[int], None]] = None):
     """Algorithm 1's loop for a batch of independent sequences.
 
     inputs_for_step(t) returns {"qkv_in": [B,W,Hq+2Hkv,D] bf16 bits} and,
@@ -320,8 +323,9 @@ def stream(win0: np.ndarray, c0: np.ndarray, steps: int,
     prefix_kv(b) returns the initial cached (k, v) of sequence b as bf16
     bits [c0, Hkv, D]; it is needed only when attention is evaluated
     (steps listed in attn_steps).  The oracle's cache keeps appended rows
-    in fp64.
-    Returns per-sequence committed tokens and slots, per-step n, final
+    in fp64; rows are rotated only where they are used (attention steps, and
+    committed rows while a cache is kept).
+    Returns per-sequence committed tokens and slots, per-step n and c, final
     window/c, and attention outputs for the requested steps.
     """
     B, W = win0.shape
@@ -330,23 +334,28 @@ def stream(win0: np.ndarray, c0: np.ndarray, steps: int,
     toks: List[List[int]] = [[] for _ in range(B)]
     slots: List[List[int]] = [[] for _ in range(B)]
     n_hist = np.zeros((steps, B), dtype=np.int64)
+    c_hist = np.zeros((steps, B), dtype=np.int64)
     sel_hist = []
     attn: Dict[int, list] = {}
-    cache_k: List[Optional[list]] = [None] * B
-    cache_v: List[Optional[list]] = [None] * B
-    if attn_steps:
+    keep_cache = len(attn_steps) > 0
+    cache_k: List[list] = [[] for _ in range(B)]
+    cache_v: List[list] = [[] for _ in range(B)]
+    if keep_cache:
         for b in range(B):
             kb, vb = prefix_kv(b)
             cache_k[b] = [bf16_to_f64(kb)]
             cache_v[b] = [bf16_to_f64(vb)]
+    last_attn = max(attn_steps) if keep_cache else -1
     for t in range(steps):
         inp = inputs_for_step(t)
         outs_t = []
         sel_t = []
         for b in range(B):
+            c_hist[t, b] = c[b]
             perm, pos, _, n_obs = reorder(win[b], c[b])
-            q, k, v = rope_window(inp["qkv_in"][b], perm, pos, Hq, Hkv, theta)
             if t in attn_steps:
+                q, k, v = rope_window(inp["qkv_in"][b], perm, pos, Hq, Hkv,
+                                      theta)
                 kp = np.concatenate(cache_k[b], axis=0)
                 vp = np.concatenate(cache_v[b], axis=0)
                 outs_t.append(window_attn(q, k, v, kp, vp)[0])
@@ -362,15 +371,23 @@ def stream(win0: np.ndarray, c0: np.ndarray, steps: int,
             slots[b] += r["slots"]
             n_hist[t, b] = r["n"]
             sel_t.append(r["selected"])
-            if attn_steps and r["n"]:
-                cache_k[b].append(k[:r["n"]])
-                cache_v[b].append(v[:r["n"]])
+            n = r["n"]
+            if keep_cache and n and t < last_attn:
+                # committed rows are physical rows 0..n-1 = logical slots
+                # 0..n-1, at positions c..c+n-1
+                _, kn, vn = rope_window(inp["qkv_in"][b], perm[:n], pos[:n],
+                                        Hq, Hkv, theta)
+                cache_k[b].append(kn)
+                cache_v[b].append(vn)
             win[b], c[b] = r["win"], r["c"]
         sel_hist.append(sel_t)
         if t in attn_steps:
             attn[t] = outs_t
-    return dict(tokens=toks, slots=slots, n=n_hist, win=np.array(win),
-                c=np.array(c), attn=attn, selected=sel_hist)
+        if progress is not None:
+            progress(t)
+    return dict(tokens=toks, slots=slots, n=n_hist, c_hist=c_hist,
+                win=np.array(win), c=np.array(c), attn=attn,
+                selected=sel_hist)
 
 
 def p_cache(n_hist: np.ndarray, W: int) -> float:

@@ -1,0 +1,203 @@
+// Algorithm 1 after the forward: commit the leftmost filled run, extend the
+// KV cache with its rows, SelectByEntropy with the distance-adjusted entropy
+// of Eq. (11), greedy Sample, and refill the window to W slots.
+//
+// One workgroup per sequence.  Wave 0 holds the window, one slot per lane:
+//   n         = count of trailing ones of the filled-slot ballot (the leading
+//               filled run in logical order; these are physical rows 0..n-1
+//               after the stable reordering);
+//   phys(s)   = n_obs + rank of mask s among the masks (Eq. 5/6 inverse);
+//   select s  iff (double)H_phys(s) < tau - lambda*(s - s0), evaluated
+//               without contraction so it rounds like the scalar reference;
+//   fallback  = argmin over masks of (double)H + lambda*(s - s0), leftmost
+//               on ties, when nothing passes and a mask exists;
+//   the new window is the filled window shifted left by n, masks appended.
+// Then every thread of the workgroup copies the n committed K and V rows
+// into their cache slots (V transposed, per the page layout).
+#include "common.h"
+
+using namespace wedlm;
+
+namespace {
+
+constexpr int kThreads = 256;
+
+struct CommitArgs {
+  int32_t* win_tok;
+  int32_t* win_start;
+  const int32_t* argmax;
+  const float* entropy;
+  double tau, lam;
+  const uint16_t* k_phys;
+  const uint16_t* v_phys;
+  uint16_t* k_cache;
+  uint16_t* v_cache;
+  int64_t num_pages;
+  const int32_t* bt;
+  int max_pages, W, Hkv, D;
+  int32_t* n_commit;
+  int32_t* committed_tok;
+  int32_t* committed_slot;
+  uint8_t* selected;
+  int32_t* status;
+};
+
+#pragma clang fp contract(off)
+__device__ __noinline__ double threshold_of(double tau, double lam, int d) {
+  return __dsub_rn(tau, __dmul_rn(lam, static_cast<double>(d)));
+}
+__device__ __noinline__ double adjusted_of(double h, double lam, int d) {
+  return __dadd_rn(h, __dmul_rn(lam, static_cast<double>(d)));
+}
+#pragma clang fp contract(on)
+
+__global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
+  const int b = blockIdx.x;
+  const int W = a.W;
+  __shared__ int s_n, s_c, s_ok;
+
+  if (threadIdx.x < kWave) {
+    const int s = threadIdx.x;
+    const bool in = s < W;
+    int t = in ? a.win_tok[b * W + s] : 0;
+    const bool is_mask = in && t < 0;
+    const uint64_t maskb = ballot(is_mask);
+    const uint64_t filledb = ballot(in && !is_mask);
+    const int n_o = __popcll(filledb);
+    const int n = maskb ? __ffsll(static_cast<long long>(maskb)) - 1 : W;
+    const int c = a.win_start[b];
+    const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
+
+    // every committed position must have a page inside the cache
+    int slot = -1, why = 0;
+    if (s < n) {
+      const int64_t p = static_cast<int64_t>(c) + s;
+      const int64_t blk = p / kPage;
+      if (c < 0 || blk >= a.max_pages) {
+        why = WEDLM_SEQ_CAPACITY;
+      } else {
+        const int id = bt[blk];
+        if (id < 0 || id >= a.num_pages) why = WEDLM_SEQ_BAD_PAGE;
+        else slot = id * kPage + static_cast<int>(p % kPage);
+      }
+    }
+    int bad = why;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) bad |= __shfl_xor(bad, off);
+
+    if (bad) {
+      if (in) {
+        a.committed_tok[b * W + s] = -1;
+        a.committed_slot[b * W + s] = -1;
+        a.selected[b * W + s] = 0;
+      }
+      if (s == 0) {
+        a.n_commit[b] = 0;
+        a.status[b] = bad;
+        s_ok = 0;
+      }
+    } else {
+      // SelectByEntropy over the mask slots (Eq. 11)
+      const int s0 = n;  // the leftmost mask ends the leading filled run
+      const int below = __popcll(maskb & ((s == 0) ? 0ull : (~0ull >> (64 - s))));
+      const int phys = n_o + below;
+      double h = 0.0;
+      int tok = 0;
+      if (is_mask) {
+        h = static_cast<double>(a.entropy[b * W + phys]);
+        tok = a.argmax[b * W + phys];
+      }
+      const int d = s - s0;
+      const bool pass = is_mask && h < threshold_of(a.tau, a.lam, d);
+      const uint64_t passb = ballot(pass);
+      bool fb = false;
+      if (passb == 0 && maskb != 0) {
+        // argmin of (adjusted entropy, slot) over the masks
+        double key = is_mask ? adjusted_of(h, a.lam, d) : __builtin_inf();
+        if (key != key) key = __builtin_inf();   // a NaN entropy ranks last
+        int who = is_mask ? s : 0x7fffffff;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+          const double k2 = __shfl_xor(key, off);
+          const int w2 = __shfl_xor(who, off);
+          if (k2 < key || (k2 == key && w2 < who)) { key = k2; who = w2; }
+        }
+        fb = s == who;
+      }
+      const bool sel = pass || fb;
+      const int filled_tok = sel ? tok : (is_mask ? WEDLM_MASK_TOKEN : t);
+      const int shifted = __shfl(filled_tok, (s + n) & (kWave - 1));
+      if (in) {
+        a.selected[b * W + s] = pass ? 1 : (fb ? 2 : 0);
+        a.committed_tok[b * W + s] = s < n ? t : -1;
+        a.committed_slot[b * W + s] = s < n ? slot : -1;
+        a.win_tok[b * W + s] = (s + n < W) ? shifted : WEDLM_MASK_TOKEN;
+      }
+      if (s == 0) {
+        a.win_start[b] = c + n;
+        a.n_commit[b] = n;
+        a.status[b] = 0;
+        s_n = n;
+        s_c = c;
+        s_ok = 1;
+      }
+    }
+  }
+  __syncthreads();
+  if (!s_ok) return;
+
+  // KV extend: physical rows 0..n-1 -> positions c..c+n-1
+  const int n = s_n, c = s_c;
+  const int D = a.D, Hkv = a.Hkv;
+  const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
+  const int per_row = Hkv * D;
+  const int total = n * per_row;
+  for (int e = threadIdx.x; e < total; e += kThreads) {
+    const int j = e / per_row;
+    const int rem = e - j * per_row;
+    const int h = rem / D;
+    const int d = rem - h * D;
+    const int p = c + j;
+    const int64_t pg = bt[p / kPage];
+    const int row = p % kPage;
+    const int64_t src = ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + d;
+    a.k_cache[((pg * Hkv + h) * kPage + row) * D + d] = a.k_phys[src];
+    a.v_cache[((pg * Hkv + h) * D + d) * kPage + row] = a.v_phys[src];
+  }
+}
+
+}  // namespace
+
+extern "C" int wedlm_commit(int32_t* win_tok, int32_t* win_start,
+                            const int32_t* argmax, const float* entropy,
+                            double tau, double lambda, const uint16_t* k_phys,
+                            const uint16_t* v_phys, uint16_t* k_cache,
+                            uint16_t* v_cache, int64_t num_pages,
+                            const int32_t* block_table, int32_t max_pages,
+                            int32_t B, int32_t W, int32_t Hkv, int32_t D,
+                            int32_t* n_commit, int32_t* committed_tok,
+                            int32_t* committed_slot, uint8_t* selected,
+                            int32_t* status, void* stream) {
+  if (!win_tok || !win_start || !argmax || !entropy || !k_phys || !v_phys ||
+      !k_cache || !v_cache || !block_table || !n_commit || !committed_tok ||
+      !committed_slot || !selected || !status)
+    return WEDLM_E_ARG;
+  if (tau != tau || lambda != lambda || num_pages < 1 || max_pages < 1)
+    return WEDLM_E_ARG;
+  if (B < 1 || B > (1 << 30) || W < 1 || W > WEDLM_MAX_WINDOW || Hkv < 1 ||
+      (D != 64 && D != 128))
+    return WEDLM_E_SHAPE;
+  if (num_pages * kPage > (1ll << 31)) return WEDLM_E_SHAPE;  // int32 slots
+  CommitArgs a{};
+  a.win_tok = win_tok; a.win_start = win_start; a.argmax = argmax;
+  a.entropy = entropy; a.tau = tau; a.lam = lambda;
+  a.k_phys = k_phys; a.v_phys = v_phys; a.k_cache = k_cache; a.v_cache = v_cache;
+  a.num_pages = num_pages; a.bt = block_table; a.max_pages = max_pages;
+  a.W = W; a.Hkv = Hkv; a.D = D;
+  a.n_commit = n_commit; a.committed_tok = committed_tok;
+  a.committed_slot = committed_slot; a.selected = selected; a.status = status;
+  hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(kThreads), 0,
+                     static_cast<hipStream_t>(stream), a);
+  WEDLM_LAUNCH_CHECK();
+  return WEDLM_OK;
+}

@@ -1,0 +1,116 @@
+// Topological reordering (Eq. 5/6) and RoPE at logical positions (Eq. 2).
+//
+// One workgroup per (physical row i, sequence b).  Wave 0 rebuilds the
+// stable partition of the window from two ballots: physical row i < n_obs
+// takes the i-th filled slot, row i >= n_obs the (i - n_obs)-th mask slot.
+// The row's angles are computed once in fp64 and shared through LDS; every
+// query and key head of the row is rotated in fp64 and rounded to bf16, the
+// value heads are copied.  The kernel moves (Hq + 2 Hkv) * D * 2 bytes in and
+// out per row; it is HBM-bound and small next to attention and scoring.
+#include "common.h"
+
+using namespace wedlm;
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxHalf = 64;   // D/2 for D <= 128
+
+__global__ __launch_bounds__(kThreads) void reorder_rope_kernel(
+    const int32_t* __restrict__ win_tok, const int32_t* __restrict__ win_start,
+    const uint16_t* __restrict__ qkv_in, int W, int Hq, int Hkv, int D,
+    double theta, int32_t* __restrict__ perm, int32_t* __restrict__ pos_ids,
+    int32_t* __restrict__ tok_phys, int32_t* __restrict__ n_obs,
+    uint16_t* __restrict__ q_phys, uint16_t* __restrict__ k_phys,
+    uint16_t* __restrict__ v_phys) {
+  const int i = blockIdx.x;
+  const int b = blockIdx.y;
+  __shared__ int s_src;
+  __shared__ double s_cos[kMaxHalf], s_sin[kMaxHalf];
+
+  if (threadIdx.x < kWave) {
+    const int s = threadIdx.x;
+    const int t = (s < W) ? win_tok[b * W + s] : 0;
+    const uint64_t filled = ballot(s < W && t >= 0);
+    const uint64_t masked = ballot(s < W && t < 0);
+    const int n_o = __popcll(filled);
+    const uint64_t bits = (i < n_o) ? filled : masked;
+    const int k = (i < n_o) ? i : i - n_o;
+    const uint64_t below = (s == 0) ? 0ull : (bits & (~0ull >> (64 - s)));
+    const bool hit = ((bits >> s) & 1ull) && __popcll(below) == k;
+    const int src = __ffsll(static_cast<long long>(ballot(hit))) - 1;
+    const int tok_src = __shfl(t, src);
+    if (s == 0) {
+      const int c = win_start[b];
+      s_src = src;
+      perm[b * W + i] = src;
+      pos_ids[b * W + i] = c + src;
+      tok_phys[b * W + i] = tok_src < 0 ? WEDLM_MASK_TOKEN : tok_src;
+      if (i == 0) n_obs[b] = n_o;
+    }
+  }
+  __syncthreads();
+  const int src = s_src;
+  const int half = D / 2;
+  if (threadIdx.x < half) {
+    const int j = threadIdx.x;
+    const double pos = static_cast<double>(win_start[b]) + src;
+    const double omega = pow(theta, -2.0 * j / D);
+    double sn, cs;
+    sincos(pos * omega, &sn, &cs);
+    s_cos[j] = cs;
+    s_sin[j] = sn;
+  }
+  __syncthreads();
+
+  const int H = Hq + 2 * Hkv;
+  const uint16_t* x = qkv_in + (static_cast<int64_t>(b) * W + src) * H * D;
+  // rotate the Hq query heads and Hkv key heads: one (head, pair) per item
+  const int n_pairs = (Hq + Hkv) * half;
+  for (int p = threadIdx.x; p < n_pairs; p += kThreads) {
+    const int head = p / half;
+    const int j = p - head * half;
+    const double a = bf16_to_f32(x[head * D + j]);
+    const double c2 = bf16_to_f32(x[head * D + j + half]);
+    const double cs = s_cos[j], sn = s_sin[j];
+    const float lo = static_cast<float>(a * cs - c2 * sn);
+    const float hi = static_cast<float>(c2 * cs + a * sn);
+    uint16_t* dst =
+        (head < Hq)
+            ? q_phys + ((static_cast<int64_t>(b) * W + i) * Hq + head) * D
+            : k_phys +
+                  ((static_cast<int64_t>(b) * W + i) * Hkv + (head - Hq)) * D;
+    dst[j] = f32_to_bf16(lo);
+    dst[j + half] = f32_to_bf16(hi);
+  }
+  // copy the value heads
+  const uint16_t* xv = x + (Hq + Hkv) * D;
+  uint16_t* dv = v_phys + (static_cast<int64_t>(b) * W + i) * Hkv * D;
+  for (int e = threadIdx.x; e < Hkv * D; e += kThreads) dv[e] = xv[e];
+}
+
+}  // namespace
+
+extern "C" int wedlm_reorder(const int32_t* win_tok, const int32_t* win_start,
+                             const uint16_t* qkv_in, int32_t B, int32_t W,
+                             int32_t Hq, int32_t Hkv, int32_t D,
+                             double rope_theta, int32_t* perm,
+                             int32_t* pos_ids, int32_t* tok_phys,
+                             int32_t* n_obs, uint16_t* q_phys,
+                             uint16_t* k_phys, uint16_t* v_phys,
+                             void* stream) {
+  if (!win_tok || !win_start || !qkv_in || !perm || !pos_ids || !tok_phys ||
+      !n_obs || !q_phys || !k_phys || !v_phys)
+    return WEDLM_E_ARG;
+  if (!(rope_theta > 1.0) || !(rope_theta < 1e300)) return WEDLM_E_ARG;
+  if (B < 1 || B > 65535 || W < 1 || W > WEDLM_MAX_WINDOW || Hkv < 1 ||
+      Hq < Hkv || Hq % Hkv != 0 || (D != 64 && D != 128) ||
+      Hq + 2 * Hkv > 1024)
+    return WEDLM_E_SHAPE;
+  hipLaunchKernelGGL(reorder_rope_kernel, dim3(W, B), dim3(kThreads), 0,
+                     static_cast<hipStream_t>(stream), win_tok, win_start,
+                     qkv_in, W, Hq, Hkv, D, rope_theta, perm, pos_ids,
+                     tok_phys, n_obs, q_phys, k_phys, v_phys);
+  WEDLM_LAUNCH_CHECK();
+  return WEDLM_OK;
+}

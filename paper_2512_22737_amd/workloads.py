@@ -137,17 +137,19 @@ def prefix_lengths(wl: Workload, seed: int = 0) -> np.ndarray:
     return np.full(wl.B, wl.prefix, dtype=np.int32)
 
 
-def pages_needed(wl: Workload, c: int) -> int:
+def pages_needed(wl: Workload, c: int, extra: int = 0) -> int:
     """Pages a sequence with prefix c needs for the whole run: its prefix,
-    every token the run can commit (at most W per step), and one window."""
-    return -(-(c + wl.steps * wl.W + wl.W) // PAGE) if wl.steps > 1 else \
-        -(-(c + wl.W) // PAGE)
+    every token the run can commit (at most W per step), one window, and
+    `extra` more positions."""
+    span = wl.steps * wl.W + wl.W if wl.steps > 1 else wl.W
+    return -(-(c + span + extra) // PAGE)
 
 
-def block_table(wl: Workload, c: np.ndarray, seed: int = 0):
+def block_table(wl: Workload, c: np.ndarray, seed: int = 0, extra: int = 0):
     """Per-sequence page lists.  Paged workloads take a seeded random
     permutation of all page ids; contiguous ones take pages in order."""
-    npg = np.array([pages_needed(wl, int(x)) for x in c], dtype=np.int64)
+    npg = np.array([pages_needed(wl, int(x), extra) for x in c],
+                   dtype=np.int64)
     total = int(npg.sum())
     if wl.paged:
         ids = rng_for(seed, wl.cid, 0, _P_TABLE).permutation(total)
@@ -197,13 +199,20 @@ def prefix_kv(wl: Workload, b: int, c: int, seed: int = 0):
 def pack_pages(wl: Workload, c: np.ndarray, bt: np.ndarray, total: int,
                seed: int = 0):
     """Scatter each sequence's logical prefix into 16-token pages.
-    K pages are [Hkv, 16, D]; V pages are [Hkv, D, 16] (transposed)."""
-    kc = np.full((total, wl.Hkv, PAGE, wl.D), BF16_NAN, dtype=np.uint16)
-    vc = np.full((total, wl.Hkv, wl.D, PAGE), BF16_NAN, dtype=np.uint16)
-    for b in range(wl.B):
+    K pages are [Hkv, 16, D]; V pages are [Hkv, D, 16] (transposed).
+    Sequences are drawn and scattered in parallel threads (each has its own
+    random stream and its own pages, so the result does not depend on the
+    threading)."""
+    from concurrent.futures import ThreadPoolExecutor
+    kc = np.empty((total, wl.Hkv, PAGE, wl.D), dtype=np.uint16)
+    vc = np.empty((total, wl.Hkv, wl.D, PAGE), dtype=np.uint16)
+    kc.fill(BF16_NAN)
+    vc.fill(BF16_NAN)
+
+    def one(b):
         cb = int(c[b])
         if cb == 0:
-            continue
+            return
         k, v = prefix_kv(wl, b, cb, seed)
         full = cb // PAGE
         pg = bt[b, :full]
@@ -217,6 +226,9 @@ def pack_pages(wl: Workload, c: np.ndarray, bt: np.ndarray, total: int,
             p = bt[b, full]
             kc[p, :, :rem, :] = k[full * PAGE:].transpose(1, 0, 2)
             vc[p, :, :, :rem] = v[full * PAGE:].transpose(1, 2, 0)
+
+    with ThreadPoolExecutor(max_workers=min(16, max(1, wl.B))) as ex:
+        list(ex.map(one, range(wl.B)))
     return kc, vc
 
 
@@ -294,18 +306,22 @@ def logits_torch(wl: Workload, pool_dev, seed: int, step: int):
 
 
 def step_inputs(wl: Workload, seed: int = 0, step: int = 0,
-                with_cache: bool = True) -> dict:
-    """Everything one single step consumes, as numpy arrays."""
+                with_cache: bool = True, extra_positions: int = 0,
+                nan_observed_rows: bool = True) -> dict:
+    """Everything one single step consumes, as numpy arrays.
+    extra_positions: more block-table room per sequence (repeated steps).
+    nan_observed_rows=False draws logits for every row."""
     c = prefix_lengths(wl, seed)
     win = initial_window(wl, seed, step)
     n_obs = (win != MASK).sum(axis=1).astype(np.int32)
-    bt, total = block_table(wl, c, seed)
+    bt, total = block_table(wl, c, seed, extra_positions)
     d = dict(win_tok=win, win_start=c.copy(), qkv_in=qkv(wl, seed, step),
              block_table=bt, num_pages=total, n_obs_gen=n_obs)
     if with_cache:
         d["k_cache"], d["v_cache"] = pack_pages(wl, c, bt, total, seed)
     if wl.steps == 1:
-        d["logits"] = logits(wl, n_obs, seed, step)
+        d["logits"] = logits(wl, n_obs if nan_observed_rows else None, seed,
+                             step)
     return d
 
 
