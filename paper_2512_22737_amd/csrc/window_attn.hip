@@ -7,20 +7,23 @@
 // positions entered only through RoPE (done by wedlm_reorder).
 //
 // Work decomposition (one GPU):
-//   workgroup = (sequence b, kv head, query block, prefix split)
-//   query block = up to 256 rows of the GQA-packed tile: row r = i*G + j is
-//                 physical window row i, query head kvh*G + j
-//   each wave owns 32 query rows; all waves share 32-key tiles of K and V
-//   staged in LDS (double-buffered through registers).
-//   S^T = K . Q^T and O^T += V^T . P^T run on v_mfma_f32_32x32x16_bf16:
-//   keys are the M dimension of the score tile, so each lane holds 16
-//   scores of ONE query column and the row max / row sum need a single
-//   cross-half exchange.  The transposed V page layout makes V^T rows
-//   contiguous, so both MFMA operands are plain LDS reads.
-//   The prefix is split so that the grid fills the 256 CUs; split partials
-//   (unnormalised O, running max and sum, log2 domain) are merged by a
-//   small combine kernel.  With a single split the main kernel normalises
-//   and writes the output itself.
+//   workgroup  = (sequence b, kv head, query block, prefix split)
+//   query rows = the GQA-packed tile: row r = i*G + j is physical window
+//                row i, query head kvh*G + j
+//   each wave owns QB blocks of 32 query rows; all waves share 32-key tiles
+//   of K and V staged in LDS.  S^T = K . Q^T and O^T += V^T . P^T run on
+//   v_mfma_f32_32x32x16_bf16: keys are the M dimension of the score tile,
+//   so a lane holds 16 scores of ONE query column and the row max / sum
+//   need one cross-half exchange; each K or V operand read from LDS feeds
+//   QB MFMAs.  The transposed V page layout makes V^T rows contiguous.
+// Latency hiding: global loads run PF tiles ahead into a ring of register
+//   stages (tile t lives in stage t % PF), so about PF * 16 KB are in flight
+//   per workgroup; the LDS tile is double-buffered, one barrier per tile.
+// Softmax: log2 domain, running max raised only when a tile's max exceeds
+//   it by more than 8 (p <= 2^8 otherwise), so the O rescale is rare.
+// Split-K: the prefix is split so that the grid fills the CUs; partials
+//   (unnormalised O, running max and sum) are merged by a combine kernel.
+//   With a single split the main kernel normalises and writes the output.
 // Roofline: the KV stream, 4 * D * Hkv bytes per prefix position, read once
 // per (sequence, kv head, query block); W*G query rows per kv head give an
 // arithmetic intensity of W*G flop/byte (256 at W=64, G=4).
@@ -31,8 +34,8 @@ using namespace wedlm;
 namespace {
 
 constexpr int kTileKeys = 32;       // keys per LDS tile (two 16-token pages)
-constexpr int kMaxWaves = 8;        // 256 query rows per workgroup
 constexpr float kLn2 = 0.69314718055994530942f;
+constexpr float kRescaleSlack = 8.0f;  // log2 units
 
 struct AttnArgs {
   const uint16_t* q;      // [B, W, Hq, D]
@@ -53,8 +56,21 @@ struct AttnArgs {
   float scale_log2;       // softmax_scale * log2(e)
 };
 
+// Kernel shape for a given number of query rows per kv head.
+struct Shape {
+  int nw, qb;             // waves per workgroup, 32-row blocks per wave
+};
+
+Shape pick_shape(int rows) {
+  if (rows <= 32) return {1, 1};
+  if (rows <= 64) return {2, 1};
+  if (rows <= 128) return {4, 1};
+  return {8, 1};
+}
+
 struct Plan {
-  int rows, nw, rows_per_wg, qblocks, rows_pad, nsplit, split_len;
+  Shape sh;
+  int rows, rows_per_wg, qblocks, rows_pad, nsplit, split_len;
   size_t ws_bytes;
 };
 
@@ -62,14 +78,13 @@ Plan make_plan(int B, int W, int Hq, int Hkv, int D, int max_prefix) {
   Plan p{};
   const int G = Hq / Hkv;
   p.rows = W * G;
-  const int blocks32 = (p.rows + 31) / 32;
-  p.nw = blocks32 >= kMaxWaves ? kMaxWaves : (blocks32 >= 4 ? 4 : (blocks32 >= 2 ? 2 : 1));
-  p.rows_per_wg = 32 * p.nw;
+  p.sh = pick_shape(p.rows);
+  p.rows_per_wg = 32 * p.sh.nw * p.sh.qb;
   p.qblocks = (p.rows + p.rows_per_wg - 1) / p.rows_per_wg;
   p.rows_pad = p.qblocks * p.rows_per_wg;
   const int tiles = (max_prefix + kTileKeys - 1) / kTileKeys;
   const int base = B * Hkv * p.qblocks;
-  const int target = 512;  // about two workgroups per CU
+  const int target = 256;   // one workgroup per CU
   int nsplit = (target + base - 1) / base;
   const int max_split = tiles / 8 > 1 ? tiles / 8 : 1;  // >= 8 tiles each
   if (nsplit > max_split) nsplit = max_split;
@@ -88,16 +103,6 @@ Plan make_plan(int B, int W, int Hq, int Hkv, int D, int max_prefix) {
   return p;
 }
 
-// LDS row pitches (elements) chosen so the MFMA operand reads are free of
-// bank conflicts: 16-byte K reads down 32 rows, 8-byte V^T reads down 32 d.
-template <int D>
-struct Lds {
-  static constexpr int kPitch = D + 8;            // K tile row: one key
-  static constexpr int vPitch = kTileKeys + 4;    // V^T tile row: one d
-  static constexpr int kElems = kTileKeys * kPitch;
-  static constexpr int vElems = D * vPitch;
-};
-
 // Sequence validity; bad lengths are reported and the sequence skipped.
 __device__ __forceinline__ bool seq_ok(const AttnArgs& a, int b, int& c) {
   c = a.plen[b];
@@ -105,171 +110,68 @@ __device__ __forceinline__ bool seq_ok(const AttnArgs& a, int b, int& c) {
          static_cast<int64_t>(c) <= static_cast<int64_t>(a.max_pages) * kPage;
 }
 
-template <int D, int NW>
-struct TileLoader {
-  static constexpr int NT = NW * kWave;
-  static constexpr int kChunksK = kTileKeys * D / 8;      // 16-byte chunks
-  static constexpr int kChunksV = kTileKeys * D / 8;
-  static constexpr int kPerThreadK = (kChunksK + NT - 1) / NT;
-  static constexpr int kPerThreadV = (kChunksV + NT - 1) / NT;
-  u16x8_t rk[kPerThreadK];
-  u16x8_t rv[kPerThreadV];
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
+typedef __attribute__((address_space(4))) const int32_t const_i32_t;
 
-  // Prefix tile: keys p0 .. p0+31, valid below k1.  Returns false and
-  // loads zeros if a page id is outside the cache.
-  __device__ bool load_prefix(const AttnArgs& a, int b, int kvh, int p0,
-                              int k1) {
-    const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
-    const int pg_idx = p0 / kPage;
-    int pg[2];
-    bool ok = true;
-    for (int h = 0; h < 2; ++h) {
-      pg[h] = -1;
-      if (p0 + h * kPage < k1) {
-        const int id = bt[pg_idx + h];
-        if (id >= 0 && id < a.num_pages) pg[h] = id;
-        else ok = false;
-      }
-    }
-    const u16x8_t zero = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-    for (int u = 0; u < kPerThreadK; ++u) {
-      const int ch = threadIdx.x + u * NT;
-      rk[u] = zero;
-      if (ch < kChunksK) {
-        const int key = ch / (D / 8);
-        const int col = ch % (D / 8);
-        const int h = key / kPage;
-        if (pg[h] >= 0 && p0 + key < k1) {
-          const uint16_t* src =
-              a.kc + ((static_cast<int64_t>(pg[h]) * a.Hkv + kvh) * kPage +
-                      (key % kPage)) * D + col * 8;
-          rk[u] = *reinterpret_cast<const u16x8_t*>(src);
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kPerThreadV; ++u) {
-      const int ch = threadIdx.x + u * NT;
-      rv[u] = zero;
-      if (ch < kChunksV) {
-        // chunk = (page half h, d, part): 8 keys of row d of that page
-        const int h = ch / (2 * D);
-        const int rem = ch % (2 * D);
-        const int d = rem / 2;
-        const int part = rem % 2;
-        if (pg[h] >= 0) {
-          const uint16_t* src =
-              a.vc + ((static_cast<int64_t>(pg[h]) * a.Hkv + kvh) * D + d) *
-                         kPage + part * 8;
-          u16x8_t v = *reinterpret_cast<const u16x8_t*>(src);
-          // zero keys at or past k1 (they may hold anything)
-          const int kbase = p0 + h * kPage + part * 8;
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (kbase + e >= k1) v[e] = 0;
-          rv[u] = v;
-        }
-      }
-    }
-    return ok;
+// Wave-uniform read of a block-table entry through the scalar cache: it
+// stays off the vector-memory counter that paces the LDS ring.
+__device__ __forceinline__ int load_uniform(const int32_t* p, int idx) {
+  idx = __builtin_amdgcn_readfirstlane(idx);
+  return ((const_i32_t*)p)[idx];
+}
+
+// s_waitcnt with only the vector-memory counter bounded by N.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (((N >> 4) & 3) << 14) | (7 << 4) |
+                             (0xF << 8));
+}
+
+// Stage layout in LDS (bytes), one 32-key tile:
+//   K   [32 keys][2D bytes]: 16-byte chunk c of key row r sits in slot
+//       c ^ swz_k(r), so the 16 lanes of one ds_read_b128 pass (16 rows,
+//       same chunk) hit 16 different slots.
+//   V^T [2 pages][D rows][32 bytes]: chunk c (8 keys) of row d sits in slot
+//       c ^ ((d >> 3) & 1); 16 lanes reading rows d..d+15 cover all banks.
+// Tiles arrive by global_load_lds_dwordx4 (1 KB per wave instruction, lane L
+// writes bytes 16L..16L+15), so each lane loads the chunk that belongs in
+// its slot.
+template <int D>
+struct Tile {
+  static constexpr int kBytes = kTileKeys * D * 2;
+  static constexpr int vBytes = kTileKeys * D * 2;
+  static constexpr int bytes = kBytes + vBytes;
+  static constexpr int nInstr = bytes / 1024;      // per tile, per workgroup
+  static constexpr int kInstr = kBytes / 1024;
+  static constexpr int keysPerInstr = 512 / D;     // K rows per instruction
+  static constexpr int vInstrPerPage = D / 32;     // V^T rows: 32 per instr
+  __device__ static __forceinline__ int swz_k(int r) {
+    return D == 128 ? (r & 15) : ((r >> 1) & 7);
   }
-
-  // Window tile: window rows j0 .. j0+31 (valid below W).
-  __device__ void load_window(const AttnArgs& a, int b, int kvh, int j0) {
-    const u16x8_t zero = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-    for (int u = 0; u < kPerThreadK; ++u) {
-      const int ch = threadIdx.x + u * NT;
-      rk[u] = zero;
-      if (ch < kChunksK) {
-        const int key = ch / (D / 8);
-        const int col = ch % (D / 8);
-        if (j0 + key < a.W) {
-          const uint16_t* src =
-              a.kw + ((static_cast<int64_t>(b) * a.W + j0 + key) * a.Hkv +
-                      kvh) * D + col * 8;
-          rk[u] = *reinterpret_cast<const u16x8_t*>(src);
-        }
-      }
-    }
-    // V rows are read token-major here and transposed on the LDS store
-#pragma unroll
-    for (int u = 0; u < kPerThreadV; ++u) {
-      const int ch = threadIdx.x + u * NT;
-      rv[u] = zero;
-      if (ch < kChunksV) {
-        const int key = ch / (D / 8);
-        const int col = ch % (D / 8);
-        if (j0 + key < a.W) {
-          const uint16_t* src =
-              a.vw + ((static_cast<int64_t>(b) * a.W + j0 + key) * a.Hkv +
-                      kvh) * D + col * 8;
-          rv[u] = *reinterpret_cast<const u16x8_t*>(src);
-        }
-      }
-    }
+  __device__ static __forceinline__ int k_off(int key, int c) {
+    return key * 2 * D + ((c ^ swz_k(key)) << 4);
   }
-
-  __device__ void store_prefix(uint16_t* kl, uint16_t* vl) const {
-#pragma unroll
-    for (int u = 0; u < kPerThreadK; ++u) {
-      const int ch = threadIdx.x + u * NT;
-      if (ch < kChunksK) {
-        const int key = ch / (D / 8);
-        const int col = ch % (D / 8);
-        *reinterpret_cast<u16x8_t*>(kl + key * Lds<D>::kPitch + col * 8) =
-            rk[u];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kPerThreadV; ++u) {
-      const int ch = threadIdx.x + u * NT;
-      if (ch < kChunksV) {
-        const int h = ch / (2 * D);
-        const int rem = ch % (2 * D);
-        const int d = rem / 2;
-        const int part = rem % 2;
-        uint16_t* dst = vl + d * Lds<D>::vPitch + h * kPage + part * 8;
-        const u16x4_t lo = {rv[u][0], rv[u][1], rv[u][2], rv[u][3]};
-        const u16x4_t hi = {rv[u][4], rv[u][5], rv[u][6], rv[u][7]};
-        *reinterpret_cast<u16x4_t*>(dst) = lo;
-        *reinterpret_cast<u16x4_t*>(dst + 4) = hi;
-      }
-    }
-  }
-
-  __device__ void store_window(uint16_t* kl, uint16_t* vl) const {
-#pragma unroll
-    for (int u = 0; u < kPerThreadK; ++u) {
-      const int ch = threadIdx.x + u * NT;
-      if (ch < kChunksK) {
-        const int key = ch / (D / 8);
-        const int col = ch % (D / 8);
-        *reinterpret_cast<u16x8_t*>(kl + key * Lds<D>::kPitch + col * 8) =
-            rk[u];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kPerThreadV; ++u) {
-      const int ch = threadIdx.x + u * NT;
-      if (ch < kChunksV) {
-        const int key = ch / (D / 8);
-        const int col = ch % (D / 8);
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          vl[(col * 8 + e) * Lds<D>::vPitch + key] = rv[u][e];
-      }
-    }
+  __device__ static __forceinline__ int v_off(int h, int d, int c) {
+    return kBytes + h * D * 32 + d * 32 + ((c ^ ((d >> 3) & 1)) << 4);
   }
 };
 
-template <int D, int NW>
+// Key row of the score tile held in MFMA output row m: bits 2 and 3 of m
+// swapped, so that output element e of a lane (hf = lane / 32) is key
+// 16*(e/8) + 8*hf + e%8 and each lane's slice of P^T is 8 contiguous keys.
+__device__ __forceinline__ int key_of_row(int m) {
+  return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+template <int D, int NW, int QB, int PF>
 __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
-  constexpr int NK = D / 16;   // k-steps of the score MFMA
-  constexpr int NM = D / 32;   // 32-row blocks of O^T
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[2][Lds<D>::kElems];
-  __shared__ __attribute__((aligned(16))) uint16_t s_v[2][Lds<D>::vElems];
+  using T = Tile<D>;
+  constexpr int NK = D / 16;          // k-steps of the score MFMA
+  constexpr int NM = D / 32;          // 32-row blocks of O^T
+  static_assert(PF >= 2, "register prefetch depth");
+  __shared__ __attribute__((aligned(1024))) char smem[3 * T::bytes];
 
   int wg = blockIdx.x;
   const int split = wg % a.nsplit;
@@ -292,160 +194,363 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   const bool last = split == nsplit_b - 1;
   const int n_pre = k1 > k0 ? (k1 - k0 + kTileKeys - 1) / kTileKeys : 0;
   const int n_win = last ? (a.W + kTileKeys - 1) / kTileKeys : 0;
-  const int n_tiles = n_pre + n_win;
 
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
   const int col = lane & 31;        // query column of this lane
   const int hf = lane >> 5;         // which half of the k slots
   const int rows = a.W * a.G;
-  const int r = qb * (NW * 32) + wave * 32 + col;
-  const bool rvalid = r < rows;
-  const int qi = rvalid ? r / a.G : 0;          // physical window row
-  const int qh = kvh * a.G + (rvalid ? r % a.G : 0);
 
-  // queries as the B operand of S^T = K . Q^T
-  bf16x8_t qf[NK];
-  {
-    const uint16_t* qp =
-        a.q + ((static_cast<int64_t>(b) * a.W + qi) * a.Hq + qh) * D;
+  // ---- register-staged loads.  A tile is 2 * 32 * D bytes in 16-byte
+  // chunks: chunk ids threadIdx.x + u * NT cover the K rows (32 keys x D/8
+  // chunks) and then the V^T rows (2 pages x D rows x 2 chunks).  Each
+  // thread's chunks have fixed offsets inside their page and inside the LDS
+  // stage, so a tile costs one page-base add per load.
+  constexpr int NT = NW * kWave;
+  constexpr int CK = kTileKeys * D / 8;
+  constexpr int CPT = 2 * CK / NT;           // chunks per thread per tile
+  static_assert(2 * CK % NT == 0, "chunks per thread");
+  int g_off[CPT], l_off[CPT], g_pg[CPT];
+  bool g_isv[CPT];
 #pragma unroll
-    for (int kk = 0; kk < NK; ++kk) {
-      u16x8_t v = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (rvalid) v = *reinterpret_cast<const u16x8_t*>(qp + kk * 16 + hf * 8);
-      qf[kk] = __builtin_bit_cast(bf16x8_t, v);
+  for (int u = 0; u < CPT; ++u) {
+    const int ch = threadIdx.x + u * NT;
+    if (ch < CK) {
+      const int key = ch / (D / 8), cc = ch % (D / 8);
+      g_isv[u] = false;
+      g_pg[u] = key / kPage;
+      g_off[u] = (key % kPage) * D + cc * 8;
+      l_off[u] = T::k_off(key, cc);
+    } else {
+      const int c2 = ch - CK;
+      const int h = c2 / (2 * D), rem = c2 % (2 * D);
+      const int d = rem / 2, part = rem % 2;
+      g_isv[u] = true;
+      g_pg[u] = h;
+      g_off[u] = d * kPage + part * 8;
+      l_off[u] = T::v_off(h, d, part);
     }
   }
-
-  floatx16_t o[NM];
-#pragma unroll
-  for (int m = 0; m < NM; ++m)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) o[m][e] = 0.f;
-  float m_run = kNegInf, l_run = 0.f;
+  const int32_t* btb = a.bt + static_cast<int64_t>(b) * a.max_pages;
   bool pages_ok = true;
-
-  TileLoader<D, NW> ld;
-  auto load_tile = [&](int t) {
-    if (t < n_pre) pages_ok &= ld.load_prefix(a, b, kvh, k0 + t * kTileKeys, k1);
-    else ld.load_window(a, b, kvh, (t - n_pre) * kTileKeys);
+  // global loads of full prefix tile t into a register stage; page ids go
+  // through the scalar cache, an invalid id is clamped to page 0 (in
+  // bounds; the sequence's status records it)
+  auto fetch = [&](int t, u16x8_t (&r)[CPT]) {
+    const int p0 = k0 + t * kTileKeys;
+    int pg[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      int id = load_uniform(btb, p0 / kPage + h);
+      if (!(id >= 0 && id < a.num_pages)) { pages_ok = false; id = 0; }
+      pg[h] = id;
+    }
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) {
+      const int64_t pbase =
+          (static_cast<int64_t>(g_pg[u] ? pg[1] : pg[0]) * a.Hkv + kvh) * kPage * D;
+      r[u] = __builtin_nontemporal_load(reinterpret_cast<const u16x8_t*>(
+          (g_isv[u] ? a.vc : a.kc) + pbase + g_off[u]));
+    }
   };
-  auto store_tile = [&](int t, int buf) {
-    if (t < n_pre) ld.store_prefix(s_k[buf], s_v[buf]);
-    else ld.store_window(s_k[buf], s_v[buf]);
+  auto stash = [&](const u16x8_t (&r)[CPT], char* sb) {
+#pragma unroll
+    for (int u = 0; u < CPT; ++u)
+      *reinterpret_cast<u16x8_t*>(sb + l_off[u]) = r[u];
   };
 
-  if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(0, 0);
+  // ---- queries (B operand of S^T = K . Q^T)
+  int qi[QB], qh[QB];
+  bool rvalid[QB];
+  bf16x8_t qf[QB][NK];
+#pragma unroll
+  for (int q = 0; q < QB; ++q) {
+    const int r = qb * (NW * QB * 32) + (wave * QB + q) * 32 + col;
+    rvalid[q] = r < rows;
+    qi[q] = rvalid[q] ? r / a.G : 0;
+    qh[q] = kvh * a.G + (rvalid[q] ? r % a.G : 0);
+    const uint16_t* qp =
+        a.q + ((static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]) * D;
+    // padded rows (past W*G) read row 0's query; their outputs are dropped
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk)
+      qf[q][kk] = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const u16x8_t*>(qp + kk * 16 + hf * 8));
   }
-  __syncthreads();
+  // take delivery of the queries here, once: later uses then see plain
+  // register values and the tile loop never waits on these loads again
+#pragma unroll
+  for (int q = 0; q < QB; ++q)
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) asm volatile("" : "+v"(qf[q][kk]));
 
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1);
-
-    // scores of 32 keys x 32 queries
-    floatx16_t acc;
+  floatx16_t o[QB][NM];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-    const uint16_t* kl = s_k[buf] + col * Lds<D>::kPitch + hf * 8;
-#pragma unroll
-    for (int kk = 0; kk < NK; ++kk) {
-      const bf16x8_t kf = __builtin_bit_cast(
-          bf16x8_t, *reinterpret_cast<const u16x8_t*>(kl + kk * 16));
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], acc, 0, 0, 0);
-    }
-
-    // mask, scale to log2 domain, online softmax
-    const bool is_win = t >= n_pre;
-    const int base = is_win ? (t - n_pre) * kTileKeys : k0 + t * kTileKeys;
-    float mx = kNegInf;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = base + (e >> 2) * 8 + hf * 4 + (e & 3);
-      const bool ok = is_win ? (key < a.W && key <= qi) : (key < k1);
-      const float s = ok ? acc[e] * a.scale_log2 : kNegInf;
-      acc[e] = s;
-      mx = fmaxf(mx, s);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float psum = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float p = __builtin_amdgcn_exp2f(acc[e] - m_use);
-      acc[e] = p;
-      psum += p;
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+  for (int q = 0; q < QB; ++q)
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) o[m][e] *= alpha;
+      for (int e = 0; e < 16; ++e) o[q][m][e] = 0.f;
+  float m_run[QB], l_run[QB];   // running max (raw score units), sum
+#pragma unroll
+  for (int q = 0; q < QB; ++q) {
+    m_run[q] = kNegInf;
+    l_run[q] = 0.f;
+  }
+  const float slack = kRescaleSlack / a.scale_log2;
 
-    // O^T += V^T . P^T, two 16-key halves of the tile
+  // ---- the three phases of one tile
+  const int krow = key_of_row(col);
+  // S^T for this wave's query columns from the K tile at stage sb
+  auto qk = [&](const char* sb, floatx16_t (&sc)[QB]) {
+#pragma unroll
+    for (int q = 0; q < QB; ++q)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[q][e] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      const bf16x8_t kf = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const u16x8_t*>(
+                        sb + T::k_off(krow, 2 * kk + hf)));
+#pragma unroll
+      for (int q = 0; q < QB; ++q)
+        sc[q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[q][kk], sc[q],
+                                                        0, 0, 0);
+    }
+  };
+  // online softmax: raw scores in, probabilities (scaled by 2^-m) out
+  auto softmax = [&](floatx16_t (&sc)[QB], bool need_mask, int base,
+                     int lim_pre, bool is_win) {
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
+      // the running max m_run stays in raw score units; the softmax scale
+      // enters once per element through p = 2^(s*c - m*c)
+      if (need_mask) {
+        const int lim = is_win ? min(a.W - 1, qi[q]) : lim_pre;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = base + 16 * (e >> 3) + 8 * hf + (e & 7);
+          sc[q][e] = key <= lim ? sc[q][e] : kNegInf;
+        }
+      }
+      float mx = fmaxf(sc[q][0], sc[q][1]);
+#pragma unroll
+      for (int e = 2; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sc[q][e], sc[q][e + 1]));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      if (ballot(mx > m_run[q] + slack)) {
+        const float m_new = fmaxf(m_run[q], mx);
+        const float alpha =
+            (m_run[q] == kNegInf)
+                ? 0.f
+                : __builtin_amdgcn_exp2f((m_run[q] - m_new) * a.scale_log2);
+        l_run[q] *= alpha;
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[q][m][e] *= alpha;
+        m_run[q] = m_new;
+      }
+      const float mc = (m_run[q] == kNegInf) ? 0.f : m_run[q] * a.scale_log2;
+      float psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float pe = __builtin_amdgcn_exp2f(
+            __builtin_fmaf(sc[q][e], a.scale_log2, -mc));
+        sc[q][e] = pe;
+        psum += pe;
+      }
+      l_run[q] += psum;
+    }
+  };
+  // O^T += V^T . P^T from the V^T tile at stage sb
+  auto pv = [&](const char* sb, const floatx16_t (&pc)[QB]) {
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
-      bf16x8_t pf;
+      bf16x8_t pf[QB];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pf[e] = static_cast<__bf16>(acc[h2 * 8 + e]);
+      for (int q = 0; q < QB; ++q)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          pf[q][e] = static_cast<__bf16>(pc[q][h2 * 8 + e]);
 #pragma unroll
       for (int m = 0; m < NM; ++m) {
-        const uint16_t* vl =
-            s_v[buf] + (m * 32 + col) * Lds<D>::vPitch + h2 * 16 + hf * 4;
-        const u16x4_t lo = *reinterpret_cast<const u16x4_t*>(vl);
-        const u16x4_t hi = *reinterpret_cast<const u16x4_t*>(vl + 8);
-        const u16x8_t vv = {lo[0], lo[1], lo[2], lo[3],
-                            hi[0], hi[1], hi[2], hi[3]};
-        o[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, vv), pf, o[m], 0, 0, 0);
+        const bf16x8_t vf = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u16x8_t*>(
+                          sb + T::v_off(h2, m * 32 + col, hf)));
+#pragma unroll
+        for (int q = 0; q < QB; ++q)
+          o[q][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[q], o[q][m],
+                                                            0, 0, 0);
       }
     }
+  };
 
-    if (t + 1 < n_tiles) store_tile(t + 1, buf ^ 1);
+  // ---- full prefix tiles.  LDS holds tiles t and t+1 (3-stage ring);
+  // tiles t+2 .. t+PF+1 are in flight in PF register stages.  Iteration t
+  // runs the score MFMAs of tile t+1, the softmax of tile t (VALU, under
+  // those MFMAs) and its P.V MFMAs, then moves tile t+2 from registers to
+  // LDS, refills that register stage with tile t+2+PF, and synchronises.
+  const bool partial_last = n_pre > 0 && (k1 - k0) % kTileKeys != 0;
+  const int n_full = n_pre - (partial_last ? 1 : 0);
+  u16x8_t rs[PF][CPT];
+  floatx16_t s_cur[QB], s_nxt[QB];
+  // Fetches and stashes are unconditional (indices past the last full tile
+  // re-read that tile; the surplus stashes land in a stage nobody reads),
+  // so the loads form one straight-line stream and every wait before a
+  // stash lets the younger tiles stay in flight.
+  const int last_full = n_full - 1;
+  if (n_full > 0) {
+#pragma unroll
+    for (int j = 0; j < PF; ++j) fetch(min(j, last_full), rs[j]);
+    stash(rs[0], smem);
+    fetch(min(PF, last_full), rs[0]);
+    stash(rs[1 % PF], smem + T::bytes);
+    fetch(min(PF + 1, last_full), rs[1 % PF]);
     __syncthreads();
+    qk(smem, s_cur);
+  }
+  constexpr int U = PF * 3;   // unroll so register and LDS stages are static
+  for (int t0 = 0; t0 < n_full; t0 += U) {
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int t = t0 + j;
+      if (t >= n_full) break;
+      const bool more = t + 1 < n_full;
+      if (more) qk(smem + ((j + 1) % 3) * T::bytes, s_nxt);
+      softmax(s_cur, false, 0, 0, false);
+      pv(smem + (j % 3) * T::bytes, s_cur);
+      stash(rs[(j + 2) % PF], smem + ((j + 2) % 3) * T::bytes);
+      fetch(min(t + 2 + PF, last_full), rs[(j + 2) % PF]);
+      __syncthreads();
+      if (more) {
+#pragma unroll
+        for (int q = 0; q < QB; ++q) s_cur[q] = s_nxt[q];
+      }
+    }
+  }
+  wait_vmcnt<0>();   // surplus fetches retire before the tail reuses stages
+
+  // ---- boundary tiles, one at a time, plain synchronous loads: the
+  // partial last prefix tile (keys past k1 or on a bad page are zeroed and
+  // masked), then the window tiles of the last split (V transposed into
+  // V^T on the store).
+  const int n_tail = (partial_last ? 1 : 0) + n_win;
+  for (int tt = 0; tt < n_tail; ++tt) {
+    const bool is_win = !(partial_last && tt == 0);
+    char* sb = smem + ((n_full + tt) % 3) * T::bytes;
+    int base, lim = 0;
+    if (!is_win) {
+      base = k0 + n_full * kTileKeys;
+      int pg[2];
+      bool pv2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int id =
+            (base + h * kPage < k1) ? load_uniform(btb, base / kPage + h) : -1;
+        pv2[h] = id >= 0 && id < a.num_pages;
+        if (base + h * kPage < k1 && !pv2[h]) pages_ok = false;
+        pg[h] = pv2[h] ? id : 0;
+      }
+      lim = !pv2[0] ? base - 1 : (!pv2[1] ? min(k1, base + kPage) - 1 : k1 - 1);
+      u16x8_t r[CPT];
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int h = g_pg[u];
+        const int64_t pbase =
+            (static_cast<int64_t>(pg[h]) * a.Hkv + kvh) * kPage * D;
+        u16x8_t v = *reinterpret_cast<const u16x8_t*>(
+            (g_isv[u] ? a.vc : a.kc) + pbase + g_off[u]);
+        // first key of this chunk: one key per K chunk, eight per V chunk
+        const int ch = threadIdx.x + u * NT;
+        const int kf = g_isv[u] ? h * kPage + ((ch - CK) % 2) * 8
+                                : ch / (D / 8);
+        const u16x8_t z = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (!g_isv[u]) {
+          v = (base + kf <= lim) ? v : z;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] = (base + kf + e <= lim) ? v[e] : static_cast<uint16_t>(0);
+        }
+        r[u] = v;
+      }
+      __syncthreads();   // every wave is done with the stage being reused
+      stash(r, sb);
+    } else {
+      base = (tt - (partial_last ? 1 : 0)) * kTileKeys;
+      __syncthreads();
+      for (int ch = threadIdx.x; ch < 2 * kTileKeys * (D / 8);
+           ch += NW * kWave) {
+        const bool isv = ch >= kTileKeys * (D / 8);
+        const int c2 = isv ? ch - kTileKeys * (D / 8) : ch;
+        const int key = c2 / (D / 8);
+        const int cc = c2 % (D / 8);
+        u16x8_t v = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (base + key < a.W)
+          v = *reinterpret_cast<const u16x8_t*>(
+              (isv ? a.vw : a.kw) +
+              ((static_cast<int64_t>(b) * a.W + base + key) * a.Hkv + kvh) * D +
+              cc * 8);
+        if (!isv) {
+          *reinterpret_cast<u16x8_t*>(sb + T::k_off(key, cc)) = v;
+        } else {
+          const int h = key / kPage, kk = key % kPage;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            *reinterpret_cast<uint16_t*>(sb + T::v_off(h, cc * 8 + e, kk / 8) +
+                                         (kk % 8) * 2) = v[e];
+        }
+      }
+    }
+    __syncthreads();
+    qk(sb, s_cur);
+    softmax(s_cur, true, base, lim, is_win);
+    pv(sb, s_cur);
   }
 
   if (!pages_ok && a.status && threadIdx.x == 0)
     atomicOr(a.status + b, WEDLM_SEQ_BAD_PAGE);
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (!rvalid) return;
-  const int64_t rows_base =
-      (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
-  if (a.nsplit == 1) {
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    uint16_t* op = a.out + ((static_cast<int64_t>(b) * a.W + qi) * a.Hq + qh) * D;
 #pragma unroll
-    for (int m = 0; m < NM; ++m)
+  for (int q = 0; q < QB; ++q) {
+    const float l_tot = l_run[q] + __shfl_xor(l_run[q], 32);
+    if (!rvalid[q]) continue;
+    const int r = qb * (NW * QB * 32) + (wave * QB + q) * 32 + col;
+    const int64_t rows_base =
+        (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
+    if (a.nsplit == 1) {
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      uint16_t* op =
+          a.out + ((static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]) * D;
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d = m * 32 + g4 * 8 + hf * 4;
-        const u16x4_t v = {f32_to_bf16(o[m][g4 * 4 + 0] * inv),
-                           f32_to_bf16(o[m][g4 * 4 + 1] * inv),
-                           f32_to_bf16(o[m][g4 * 4 + 2] * inv),
-                           f32_to_bf16(o[m][g4 * 4 + 3] * inv)};
-        *reinterpret_cast<u16x4_t*>(op + d) = v;
-      }
-    if (a.lse && hf == 0)
-      a.lse[(static_cast<int64_t>(b) * a.W + qi) * a.Hq + qh] =
-          (m_run + __log2f(l_tot)) * kLn2;
-  } else {
-    float* wp = a.ws_o + (rows_base * a.nsplit + split) * D;
+      for (int m = 0; m < NM; ++m)
 #pragma unroll
-    for (int m = 0; m < NM; ++m)
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const int d = m * 32 + g4 * 8 + hf * 4;
+          const u16x4_t v = {f32_to_bf16(o[q][m][g4 * 4 + 0] * inv),
+                             f32_to_bf16(o[q][m][g4 * 4 + 1] * inv),
+                             f32_to_bf16(o[q][m][g4 * 4 + 2] * inv),
+                             f32_to_bf16(o[q][m][g4 * 4 + 3] * inv)};
+          *reinterpret_cast<u16x4_t*>(op + d) = v;
+        }
+      if (a.lse && hf == 0)
+        a.lse[(static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]] =
+            (m_run[q] * a.scale_log2 + __log2f(l_tot)) * kLn2;
+    } else {
+      float* wp = a.ws_o + (rows_base * a.nsplit + split) * D;
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d = m * 32 + g4 * 8 + hf * 4;
-        const floatx4_t v = {o[m][g4 * 4 + 0], o[m][g4 * 4 + 1],
-                             o[m][g4 * 4 + 2], o[m][g4 * 4 + 3]};
-        *reinterpret_cast<floatx4_t*>(wp + d) = v;
-      }
-    if (hf == 0) a.ws_ml[rows_base * a.nsplit + split] = make_float2(m_run, l_tot);
+      for (int m = 0; m < NM; ++m)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const int d = m * 32 + g4 * 8 + hf * 4;
+          const floatx4_t v = {o[q][m][g4 * 4 + 0], o[q][m][g4 * 4 + 1],
+                               o[q][m][g4 * 4 + 2], o[q][m][g4 * 4 + 3]};
+          *reinterpret_cast<floatx4_t*>(wp + d) = v;
+        }
+      if (hf == 0)
+        a.ws_ml[rows_base * a.nsplit + split] =
+            make_float2(m_run[q] * a.scale_log2, l_tot);   // log2 units
+    }
   }
 }
 
@@ -489,18 +594,22 @@ __global__ __launch_bounds__(D) void attn_combine_kernel(AttnArgs a) {
 template <int D>
 int launch(const AttnArgs& a, const Plan& p, hipStream_t st) {
   const int grid = a.nsplit * a.B * a.Hkv * a.qblocks;
-  switch (p.nw) {
+  switch (p.sh.nw) {
     case 8:
-      hipLaunchKernelGGL((window_attn_kernel<D, 8>), dim3(grid), dim3(8 * kWave), 0, st, a);
+      hipLaunchKernelGGL((window_attn_kernel<D, 8, 1, 3>), dim3(grid),
+                         dim3(8 * kWave), 0, st, a);
       break;
     case 4:
-      hipLaunchKernelGGL((window_attn_kernel<D, 4>), dim3(grid), dim3(4 * kWave), 0, st, a);
+      hipLaunchKernelGGL((window_attn_kernel<D, 4, 1, 3>), dim3(grid),
+                         dim3(4 * kWave), 0, st, a);
       break;
     case 2:
-      hipLaunchKernelGGL((window_attn_kernel<D, 2>), dim3(grid), dim3(2 * kWave), 0, st, a);
+      hipLaunchKernelGGL((window_attn_kernel<D, 2, 1, 2>), dim3(grid),
+                         dim3(2 * kWave), 0, st, a);
       break;
     default:
-      hipLaunchKernelGGL((window_attn_kernel<D, 1>), dim3(grid), dim3(kWave), 0, st, a);
+      hipLaunchKernelGGL((window_attn_kernel<D, 1, 1, 2>), dim3(grid),
+                         dim3(kWave), 0, st, a);
       break;
   }
   WEDLM_LAUNCH_CHECK();
