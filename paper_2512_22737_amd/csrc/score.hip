@@ -24,72 +24,123 @@ using namespace wedlm;
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kBlk = 16;                 // logits per thread per step
 constexpr double kLn2 = 0.69314718055994530942;
 
+// Partial result over a set of logits, relative to its maximum m:
+//   R = sum over x < m of 2^y,  S = sum over x < m of -y 2^y  (log2 units),
+//   y = (x - m) * log2(e) / T, ties = number of logits equal to m,
+//   tok = lowest index holding m.
+// The entropy needs R' = R + ties - 1 (all terms but the argmax); keeping
+// the ties as an exact count avoids subtracting the argmax's 1 from a sum.
 struct State {
-  float m;      // max logit
-  int tok;      // its lowest index
-  double R;     // sum over v != tok of 2^{y_v}
-  double S;     // sum over v != tok of -y_v 2^{y_v}  (log2 units)
+  float m;
+  int tok;
+  int ties;
+  double R, S;
 };
 
 __device__ __forceinline__ State empty_state() {
-  return State{kNegInf, 0x7fffffff, 0.0, 0.0};
+  return State{kNegInf, 0x7fffffff, 0, 0.0, 0.0};
 }
 
-// 2^y for y <= 0 (fp64 argument), relative error ~1 fp32 ulp; 0 below -200.
-__device__ __forceinline__ double exp2_acc(double y) {
-  if (!(y > -200.0)) return 0.0;
+// 2^y for y <= 0 given in fp64: v_exp_f32 on the fp32 head, the tail as a
+// first-order correction; relative error about one fp32 ulp.  Zero below
+// -200 (where the fp32 exponential underflows anyway).  Callers clamp y at
+// -256 so that a -inf logit adds 0 (not inf * 0) to S.
+__device__ __forceinline__ float exp2_split(double y) {
   const float yh = static_cast<float>(y);
-  const double yl = y - static_cast<double>(yh);
-  const double e = static_cast<double>(__builtin_amdgcn_exp2f(yh));
-  return __fma_rn(e, yl * kLn2, e);
+  const float yl = static_cast<float>((y - static_cast<double>(yh)) * kLn2);
+  const float e = __builtin_amdgcn_exp2f(yh);
+  return y > -200.0 ? __builtin_fmaf(e, yl, e) : 0.f;
 }
 
-// Add one element (value x at index v) to a state.  c2 = log2(e) / T.
-__device__ __forceinline__ void push(State& st, float x, int v, double c2) {
-  if (x > st.m) {
-    if (st.m != kNegInf) {
-      // the old maximum joins the sums; every old term shifts by dy < 0
-      const double dy = (static_cast<double>(st.m) - x) * c2;
-      const double e = exp2_acc(dy);
-      st.S = e * (st.S - dy * (st.R + 1.0));
-      st.R = e * (st.R + 1.0);
-      if (e == 0.0) st.S = 0.0;
-    }
-    st.m = x;
-    st.tok = v;
-  } else {
-    const double y = (static_cast<double>(x) - st.m) * c2;
-    const double e = exp2_acc(y);
-    st.R += e;
-    if (e > 0.0) st.S = __fma_rn(-y, e, st.S);
-  }
+// Re-express state st relative to a larger maximum: every old term, the old
+// ties included, shifts by dy = (m_old - m_new) * c2 < 0.
+__device__ __forceinline__ void shift_state(State& st, float m_new, double c2) {
+  if (st.m == kNegInf) { st.R = 0.0; st.S = 0.0; st.ties = 0; return; }
+  const double dy = (static_cast<double>(st.m) - m_new) * c2;
+  const double all = st.R + st.ties;
+  const double e = static_cast<double>(exp2_split(dy));
+  st.S = e > 0.0 ? e * (st.S - dy * all) : 0.0;
+  st.R = e * all;
+  st.ties = 0;
 }
 
-// Merge state o into st.  The winner keeps its maximum; the loser's terms,
-// its own maximum included, shift by dy = (m_loser - m_winner) * c2 <= 0.
-__device__ __forceinline__ void merge(State& st, const State& o, double c2) {
+// Merge o into st (associative up to rounding; ties keep the lower index).
+__device__ __forceinline__ void merge(State& st, State o, double c2) {
   if (o.m == kNegInf) return;
   if (st.m == kNegInf) { st = o; return; }
-  const bool keep = (st.m > o.m) || (st.m == o.m && st.tok < o.tok);
-  const State& w = keep ? st : o;
-  const State& l = keep ? o : st;
-  const double dy = (static_cast<double>(l.m) - w.m) * c2;
-  const double e = exp2_acc(dy);
-  double R = w.R + e * (l.R + 1.0);
-  double S = w.S;
-  if (e > 0.0) S += e * (l.S - dy * (l.R + 1.0));
-  st = State{w.m, w.tok, R, S};
+  if (o.m > st.m) shift_state(st, o.m, c2);
+  else if (st.m > o.m) shift_state(o, st.m, c2);
+  State r;
+  r.m = st.m > o.m ? st.m : o.m;
+  r.tok = (st.m == r.m && o.m == r.m) ? min(st.tok, o.tok)
+                                      : (st.m == r.m ? st.tok : o.tok);
+  r.ties = st.ties + o.ties;
+  r.R = st.R + o.R;
+  r.S = st.S + o.S;
+  st = r;
 }
 
 __device__ __forceinline__ State shfl_xor_state(const State& s, int mask) {
   State o;
   o.m = __shfl_xor(s.m, mask);
   o.tok = __shfl_xor(s.tok, mask);
+  o.ties = __shfl_xor(s.ties, mask);
   o.R = __shfl_xor(s.R, mask);
   o.S = __shfl_xor(s.S, mask);
   return o;
+}
+
+// Add a block of n logits x[k] at indices idx[k] (increasing) to st.
+// Fast path (no logit reaches the running max): fixed reference, no
+// compares.  Otherwise: raise the max if needed, then count ties.
+template <int N>
+__device__ __forceinline__ void push_block(State& st, const float (&x)[N],
+                                           const int (&idx)[N], double c2) {
+  float bm = x[0];
+#pragma unroll
+  for (int k = 1; k < N; ++k) bm = fmaxf(bm, x[k]);
+  const double mc = static_cast<double>(st.m) * c2;
+  if (bm < st.m) {
+    float r = 0.f, sy = 0.f;
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const double y =
+          fmax(__builtin_fma(static_cast<double>(x[k]), c2, -mc), -256.0);
+      const float e = exp2_split(y);
+      r += e;
+      sy = __builtin_fmaf(-static_cast<float>(y), e, sy);
+    }
+    st.R += r;
+    st.S += sy;
+    return;
+  }
+  if (bm > st.m) {
+    shift_state(st, bm, c2);
+    st.m = bm;
+    int t = 0x7fffffff;
+#pragma unroll
+    for (int k = N - 1; k >= 0; --k) t = (x[k] == bm) ? idx[k] : t;
+    st.tok = t;
+  }
+  const double mc2 = static_cast<double>(st.m) * c2;
+  float r = 0.f, sy = 0.f;
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    if (x[k] == st.m) {
+      st.ties += 1;
+    } else {
+      const double y =
+          fmax(__builtin_fma(static_cast<double>(x[k]), c2, -mc2), -256.0);
+      const float e = exp2_split(y);
+      r += e;
+      sy = __builtin_fmaf(-static_cast<float>(y), e, sy);
+    }
+  }
+  st.R += r;
+  st.S += sy;
 }
 
 // Reduce the block's states into thread 0's.
@@ -109,11 +160,12 @@ __device__ State block_reduce(State st, double c2) {
 __device__ __forceinline__ void finish(const State& st, int64_t idx,
                                        int32_t* argmax, float* entropy,
                                        float* pmax) {
+  const double R = st.R + (st.ties - 1);   // every term but the argmax
   const double S = st.S * kLn2;            // back to nats
-  const double H = log1p(st.R) + S / (1.0 + st.R);
+  const double H = log1p(R) + S / (1.0 + R);
   argmax[idx] = st.m == kNegInf ? 0 : st.tok;   // an all -inf row: id 0
   entropy[idx] = static_cast<float>(H);
-  if (pmax) pmax[idx] = static_cast<float>(1.0 / (1.0 + st.R));
+  if (pmax) pmax[idx] = static_cast<float>(1.0 / (1.0 + R));
 }
 
 struct ScoreArgs {
@@ -130,6 +182,7 @@ struct ScoreArgs {
 
 // kVec: rows start on 16-byte boundaries (row_stride % 4 == 0 and an
 // aligned base), so the body streams 16-byte loads; otherwise 4-byte loads.
+// Thread t takes float4 groups t, t+256, ... of the chunk, four at a time.
 template <bool kVec>
 __global__ __launch_bounds__(kThreads) void score_kernel(ScoreArgs a) {
   const int ch = blockIdx.x % a.nchunk;
@@ -143,18 +196,33 @@ __global__ __launch_bounds__(kThreads) void score_kernel(ScoreArgs a) {
   const int v0 = ch * a.chunk;
   const int v1 = min(a.V, v0 + a.chunk);
   State st = empty_state();
-  // chunk bounds are multiples of 4 elements, the row tail may not be
-  const int v1v = kVec ? v0 + ((v1 - v0) & ~3) : v0;
+  constexpr int kStep = kThreads * kBlk;       // logits per workgroup step
+  int v = v0;
   if (kVec) {
-    for (int v = v0 + threadIdx.x * 4; v < v1v; v += kThreads * 4) {
-      const floatx4_t q = *reinterpret_cast<const floatx4_t*>(x + v);
-      push(st, q[0], v, a.c2);
-      push(st, q[1], v + 1, a.c2);
-      push(st, q[2], v + 2, a.c2);
-      push(st, q[3], v + 3, a.c2);
+    for (; v + kStep <= v1; v += kStep) {
+      float xs[kBlk];
+      int idx[kBlk];
+#pragma unroll
+      for (int g = 0; g < kBlk / 4; ++g) {
+        const int vg = v + (g * kThreads + threadIdx.x) * 4;
+        const floatx4_t q = __builtin_nontemporal_load(
+            reinterpret_cast<const floatx4_t*>(x + vg));
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          xs[g * 4 + k] = q[k];
+          idx[g * 4 + k] = vg + k;
+        }
+      }
+      push_block(st, xs, idx, a.c2);
     }
   }
-  for (int v = v1v + threadIdx.x; v < v1; v += kThreads) push(st, x[v], v, a.c2);
+  // remainder (and the whole chunk without 16-byte alignment): one logit at
+  // a time in increasing index order per thread
+  for (int u = v + threadIdx.x; u < v1; u += kThreads) {
+    const float xs[1] = {x[u]};
+    const int idx[1] = {u};
+    push_block(st, xs, idx, a.c2);
+  }
   st = block_reduce(st, a.c2);
   if (threadIdx.x != 0) return;
   if (a.nchunk == 1) finish(st, row, a.argmax, a.entropy, a.pmax);

@@ -113,6 +113,20 @@ __device__ __forceinline__ bool seq_ok(const AttnArgs& a, int b, int& c) {
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 typedef __attribute__((address_space(4))) const int32_t const_i32_t;
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Word 3 of a raw buffer resource on gfx950 (32-bit data format, no
+// swizzle); reads past num_records return zero.
+constexpr int kBufferFlags = 0x00020000;
+
+// Values of x in this lane and in the lane 32 away (v_permlane32_swap).
+__device__ __forceinline__ void xor32_pair(float x, float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                                  __float_as_uint(x), false,
+                                                  false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
 
 // Wave-uniform read of a block-table entry through the scalar cache: it
 // stays off the vector-memory counter that paces the LDS ring.
@@ -201,38 +215,33 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   const int hf = lane >> 5;         // which half of the k slots
   const int rows = a.W * a.G;
 
-  // ---- register-staged loads.  A tile is 2 * 32 * D bytes in 16-byte
-  // chunks: chunk ids threadIdx.x + u * NT cover the K rows (32 keys x D/8
-  // chunks) and then the V^T rows (2 pages x D rows x 2 chunks).  Each
-  // thread's chunks have fixed offsets inside their page and inside the LDS
-  // stage, so a tile costs one page-base add per load.
+  // ---- register-staged loads.  A tile is four 4 KB blocks (D = 128; 2 KB
+  // for D = 64): the K rows of page 0 and page 1, then the V^T rows of page
+  // 0 and page 1, each contiguous in the cache.  Chunk g = wave*64*CPT +
+  // u*64 + lane (16 bytes) belongs to block g / BC, so the block of a
+  // (wave, u) pair is wave-uniform: every load is a raw buffer load through
+  // a per-page resource (scalar registers) at a fixed per-lane offset, and
+  // lands at a fixed per-lane LDS offset.
   constexpr int NT = NW * kWave;
-  constexpr int CK = kTileKeys * D / 8;
-  constexpr int CPT = 2 * CK / NT;           // chunks per thread per tile
-  static_assert(2 * CK % NT == 0, "chunks per thread");
-  int g_off[CPT], l_off[CPT], g_pg[CPT];
-  bool g_isv[CPT];
+  constexpr int BC = kPage * D / 8;          // 16-byte chunks per block
+  constexpr int CPT = 4 * BC / NT;           // chunks per thread per tile
+  static_assert(4 * BC % NT == 0 && (64 * CPT) % 64 == 0, "chunk split");
+  int g_voff[CPT], l_off[CPT], g_blk[CPT];
 #pragma unroll
   for (int u = 0; u < CPT; ++u) {
-    const int ch = threadIdx.x + u * NT;
-    if (ch < CK) {
-      const int key = ch / (D / 8), cc = ch % (D / 8);
-      g_isv[u] = false;
-      g_pg[u] = key / kPage;
-      g_off[u] = (key % kPage) * D + cc * 8;
-      l_off[u] = T::k_off(key, cc);
+    const int g = wave * 64 * CPT + u * 64 + lane;
+    const int blk = g / BC, c = g % BC;
+    g_blk[u] = __builtin_amdgcn_readfirstlane(blk);
+    g_voff[u] = c * 16;
+    if (blk < 2) {
+      l_off[u] = T::k_off(blk * kPage + c / (D / 8), c % (D / 8));
     } else {
-      const int c2 = ch - CK;
-      const int h = c2 / (2 * D), rem = c2 % (2 * D);
-      const int d = rem / 2, part = rem % 2;
-      g_isv[u] = true;
-      g_pg[u] = h;
-      g_off[u] = d * kPage + part * 8;
-      l_off[u] = T::v_off(h, d, part);
+      l_off[u] = T::v_off(blk - 2, c / 2, c % 2);
     }
   }
   const int32_t* btb = a.bt + static_cast<int64_t>(b) * a.max_pages;
   bool pages_ok = true;
+  constexpr int kBlockBytes = kPage * D * 2;
   // global loads of full prefix tile t into a register stage; page ids go
   // through the scalar cache, an invalid id is clamped to page 0 (in
   // bounds; the sequence's status records it)
@@ -247,10 +256,15 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
     }
 #pragma unroll
     for (int u = 0; u < CPT; ++u) {
-      const int64_t pbase =
-          (static_cast<int64_t>(g_pg[u] ? pg[1] : pg[0]) * a.Hkv + kvh) * kPage * D;
-      r[u] = __builtin_nontemporal_load(reinterpret_cast<const u16x8_t*>(
-          (g_isv[u] ? a.vc : a.kc) + pbase + g_off[u]));
+      const int blk = g_blk[u];
+      const int h = blk & 1;
+      const uint16_t* base = ((blk < 2) ? a.kc : a.vc) +
+                             (static_cast<int64_t>(h ? pg[1] : pg[0]) * a.Hkv + kvh) *
+                                 kPage * D;
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(base), 0, kBlockBytes, kBufferFlags);
+      r[u] = __builtin_bit_cast(
+          u16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, g_voff[u], 0, 0));
     }
   };
   auto stash = [&](const u16x8_t (&r)[CPT], char* sb) {
@@ -318,9 +332,11 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
                                                         0, 0, 0);
     }
   };
-  // online softmax: raw scores in, probabilities (scaled by 2^-m) out
-  auto softmax = [&](floatx16_t (&sc)[QB], bool need_mask, int base,
-                     int lim_pre, bool is_win) {
+  // online softmax, first half: mask, tile max, lazily raised running
+  // max (rescaling O and l when it rises by more than the slack).  Returns
+  // the scaled max m*c that the exponentials subtract.
+  auto softmax_max = [&](floatx16_t (&sc)[QB], bool need_mask, int base,
+                         int lim_pre, bool is_win, float (&mc)[QB]) {
 #pragma unroll
     for (int q = 0; q < QB; ++q) {
       // the running max m_run stays in raw score units; the softmax scale
@@ -336,7 +352,11 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
       float mx = fmaxf(sc[q][0], sc[q][1]);
 #pragma unroll
       for (int e = 2; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sc[q][e], sc[q][e + 1]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      {
+        float x0, x1;
+        xor32_pair(mx, x0, x1);
+        mx = fmaxf(x0, x1);
+      }
       if (ballot(mx > m_run[q] + slack)) {
         const float m_new = fmaxf(m_run[q], mx);
         const float alpha =
@@ -350,39 +370,56 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
           for (int e = 0; e < 16; ++e) o[q][m][e] *= alpha;
         m_run[q] = m_new;
       }
-      const float mc = (m_run[q] == kNegInf) ? 0.f : m_run[q] * a.scale_log2;
-      float psum = 0.f;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float pe = __builtin_amdgcn_exp2f(
-            __builtin_fmaf(sc[q][e], a.scale_log2, -mc));
-        sc[q][e] = pe;
-        psum += pe;
-      }
-      l_run[q] += psum;
+      mc[q] = (m_run[q] == kNegInf) ? 0.f : m_run[q] * a.scale_log2;
     }
   };
-  // O^T += V^T . P^T from the V^T tile at stage sb
-  auto pv = [&](const char* sb, const floatx16_t (&pc)[QB]) {
+  // second half: p = 2^(s*c - m*c), the row sum, and P^T in bf16 as the B
+  // operand of the two 16-key P.V MFMAs.  Straight-line VALU only.
+  auto softmax_exp = [&](const floatx16_t (&sc)[QB], const float (&mc)[QB],
+                         bf16x8_t (&pf)[QB][2]) {
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      bf16x8_t pf[QB];
+    for (int q = 0; q < QB; ++q) {
+      float pe[16];
 #pragma unroll
-      for (int q = 0; q < QB; ++q)
+      for (int e = 0; e < 16; ++e)
+        pe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[q][e], a.scale_log2, -mc[q]));
+      float ps[4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          pf[q][e] = static_cast<__bf16>(pc[q][h2 * 8 + e]);
+      for (int g = 0; g < 4; ++g)
+        ps[g] = (pe[4 * g] + pe[4 * g + 1]) + (pe[4 * g + 2] + pe[4 * g + 3]);
+      l_run[q] += (ps[0] + ps[1]) + (ps[2] + ps[3]);
 #pragma unroll
-      for (int m = 0; m < NM; ++m) {
-        const bf16x8_t vf = __builtin_bit_cast(
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[q][h2][e] = static_cast<__bf16>(pe[h2 * 8 + e]);
+    }
+  };
+  auto softmax = [&](floatx16_t (&sc)[QB], bool need_mask, int base,
+                     int lim_pre, bool is_win, bf16x8_t (&pf)[QB][2]) {
+    float mc[QB];
+    softmax_max(sc, need_mask, base, lim_pre, is_win, mc);
+    softmax_exp(sc, mc, pf);
+  };
+  // V^T fragments of a tile: the A operands of the P.V MFMAs
+  auto vread = [&](const char* sb, bf16x8_t (&vf)[2][NM]) {
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+        vf[h2][m] = __builtin_bit_cast(
             bf16x8_t, *reinterpret_cast<const u16x8_t*>(
                           sb + T::v_off(h2, m * 32 + col, hf)));
+  };
+  // O^T += V^T . P^T
+  auto pv = [&](const bf16x8_t (&vf)[2][NM], const bf16x8_t (&pf)[QB][2]) {
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
 #pragma unroll
         for (int q = 0; q < QB; ++q)
-          o[q][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[q], o[q][m],
-                                                            0, 0, 0);
-      }
-    }
+          o[q][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[h2][m], pf[q][h2],
+                                                            o[q][m], 0, 0, 0);
   };
 
   // ---- full prefix tiles.  LDS holds tiles t and t+1 (3-stage ring);
@@ -393,7 +430,7 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   const bool partial_last = n_pre > 0 && (k1 - k0) % kTileKeys != 0;
   const int n_full = n_pre - (partial_last ? 1 : 0);
   u16x8_t rs[PF][CPT];
-  floatx16_t s_cur[QB], s_nxt[QB];
+  floatx16_t sbuf[2][QB];     // scores of tile t in sbuf[t & 1]
   // Fetches and stashes are unconditional (indices past the last full tile
   // re-read that tile; the surplus stashes land in a stage nobody reads),
   // so the loads form one straight-line stream and every wait before a
@@ -407,26 +444,53 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
     stash(rs[1 % PF], smem + T::bytes);
     fetch(min(PF + 1, last_full), rs[1 % PF]);
     __syncthreads();
-    qk(smem, s_cur);
+    qk(smem, sbuf[0]);
   }
-  constexpr int U = PF * 3;   // unroll so register and LDS stages are static
+  {
+  // unroll so register stages, LDS stages and score buffers are static
+  constexpr int U = (PF % 2 == 0 ? PF : 2 * PF) * (PF % 3 == 0 ? 1 : 3);
   for (int t0 = 0; t0 < n_full; t0 += U) {
 #pragma unroll
     for (int j = 0; j < U; ++j) {
       const int t = t0 + j;
       if (t >= n_full) break;
-      const bool more = t + 1 < n_full;
-      if (more) qk(smem + ((j + 1) % 3) * T::bytes, s_nxt);
-      softmax(s_cur, false, 0, 0, false);
-      pv(smem + (j % 3) * T::bytes, s_cur);
+      // K fragments of tile t+1 (past the last full tile the stage holds a
+      // re-read tile; that score block is never used)
+      const char* sk = smem + ((j + 1) % 3) * T::bytes;
+      bf16x8_t kf[NK];
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk)
+        kf[kk] = __builtin_bit_cast(
+            bf16x8_t,
+            *reinterpret_cast<const u16x8_t*>(sk + T::k_off(krow, 2 * kk + hf)));
+      bf16x8_t vf[2][NM];
+      vread(smem + (j % 3) * T::bytes, vf);
+      float mc[QB];
+      softmax_max(sbuf[j & 1], false, 0, 0, false, mc);
+      // one scheduling region: the score MFMAs of tile t+1 interleaved with
+      // the exponentials of tile t
+      bf16x8_t pf[QB][2];
+#pragma unroll
+      for (int q = 0; q < QB; ++q) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sbuf[(j + 1) & 1][q][e] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk)
+          sbuf[(j + 1) & 1][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              kf[kk], qf[q][kk], sbuf[(j + 1) & 1][q], 0, 0, 0);
+      }
+      softmax_exp(sbuf[j & 1], mc, pf);
+#pragma unroll
+      for (int i = 0; i < NK * QB; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // six VALU
+      }
+      pv(vf, pf);
       stash(rs[(j + 2) % PF], smem + ((j + 2) % 3) * T::bytes);
       fetch(min(t + 2 + PF, last_full), rs[(j + 2) % PF]);
       __syncthreads();
-      if (more) {
-#pragma unroll
-        for (int q = 0; q < QB; ++q) s_cur[q] = s_nxt[q];
-      }
     }
+  }
   }
   wait_vmcnt<0>();   // surplus fetches retire before the tail reuses stages
 
@@ -455,17 +519,18 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
       u16x8_t r[CPT];
 #pragma unroll
       for (int u = 0; u < CPT; ++u) {
-        const int h = g_pg[u];
+        const int blk = g_blk[u];
+        const int h = blk & 1;
+        const bool isv = blk >= 2;
         const int64_t pbase =
             (static_cast<int64_t>(pg[h]) * a.Hkv + kvh) * kPage * D;
         u16x8_t v = *reinterpret_cast<const u16x8_t*>(
-            (g_isv[u] ? a.vc : a.kc) + pbase + g_off[u]);
+            (isv ? a.vc : a.kc) + pbase + g_voff[u] / 2);
         // first key of this chunk: one key per K chunk, eight per V chunk
-        const int ch = threadIdx.x + u * NT;
-        const int kf = g_isv[u] ? h * kPage + ((ch - CK) % 2) * 8
-                                : ch / (D / 8);
+        const int c = g_voff[u] / 16;
+        const int kf = isv ? h * kPage + (c % 2) * 8 : h * kPage + c / (D / 8);
         const u16x8_t z = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (!g_isv[u]) {
+        if (!isv) {
           v = (base + kf <= lim) ? v : z;
         } else {
 #pragma unroll
@@ -503,9 +568,11 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
       }
     }
     __syncthreads();
-    qk(sb, s_cur);
-    softmax(s_cur, true, base, lim, is_win);
-    pv(sb, s_cur);
+    qk(sb, sbuf[0]);
+    bf16x8_t pf[QB][2], vf[2][NM];
+    softmax(sbuf[0], true, base, lim, is_win, pf);
+    vread(sb, vf);
+    pv(vf, pf);
   }
 
   if (!pages_ok && a.status && threadIdx.x == 0)
@@ -513,7 +580,9 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
 
 #pragma unroll
   for (int q = 0; q < QB; ++q) {
-    const float l_tot = l_run[q] + __shfl_xor(l_run[q], 32);
+    float l0, l1;
+    xor32_pair(l_run[q], l0, l1);
+    const float l_tot = l0 + l1;
     if (!rvalid[q]) continue;
     const int r = qb * (NW * QB * 32) + (wave * QB + q) * 32 + col;
     const int64_t rows_base =
