@@ -126,3 +126,12 @@ def test_capacity_error_leaves_state():
     assert (g["win_tok"] == d["win_tok"]).all()
     assert (g["win_start"] == d["win_start"]).all()
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("lam,temp", [(0.1, 0.1), (0.01, 1.0)])
+def test_secondary_readings(lam, temp):
+    """The paper's default lambda = 0.1, and the entropy at T = 1 (where the
+    threshold almost never passes and the fallback fills one mask)."""
+    for name in ("tiny", "qwen3_8b_layer"):
+        wl = WL.WORKLOADS[name].replace(lam=lam, temp=temp)
+        _full_check(wl, WL.step_inputs(wl, seed=3))
