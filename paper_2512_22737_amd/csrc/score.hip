@@ -55,6 +55,18 @@ __device__ __forceinline__ float exp2_split(double y) {
   return y > -200.0 ? __builtin_fmaf(e, yl, e) : 0.f;
 }
 
+// One term of the sums: 2^y with y = x*c2 - mc formed in fp64 and clamped
+// at -256 (a -inf logit gives 0, never inf * 0), then split into an fp32
+// head yh (returned, for the S sum) and tail for exp2_split's correction.
+__device__ __forceinline__ float exp2_term(float x, double c2, double mc,
+                                           float& yh) {
+  const double y = fmax(__builtin_fma(static_cast<double>(x), c2, -mc), -256.0);
+  yh = static_cast<float>(y);
+  const float yl = static_cast<float>(y - static_cast<double>(yh));
+  const float e = __builtin_amdgcn_exp2f(yh);   // 0 below about -150
+  return __builtin_fmaf(e * static_cast<float>(kLn2), yl, e);
+}
+
 // Re-express state st relative to a larger maximum: every old term, the old
 // ties included, shifts by dy = (m_old - m_new) * c2 < 0.
 __device__ __forceinline__ void shift_state(State& st, float m_new, double c2) {
@@ -93,30 +105,17 @@ __device__ __forceinline__ State shfl_xor_state(const State& s, int mask) {
   return o;
 }
 
-// Add a block of n logits x[k] at indices idx[k] (increasing) to st.
-// Fast path (no logit reaches the running max): fixed reference, no
-// compares.  Otherwise: raise the max if needed, then count ties.
+// Add a block of n logits x[k] at indices idx[k] (increasing) to st.  A
+// block whose maximum exceeds the running max first raises it (rescaling
+// the sums); then every logit adds its term, except those equal to the
+// max, which are counted as ties instead (their term is exactly 1 and is
+// never summed, so nothing cancels later).
 template <int N>
 __device__ __forceinline__ void push_block(State& st, const float (&x)[N],
                                            const int (&idx)[N], double c2) {
   float bm = x[0];
 #pragma unroll
   for (int k = 1; k < N; ++k) bm = fmaxf(bm, x[k]);
-  const double mc = static_cast<double>(st.m) * c2;
-  if (bm < st.m) {
-    float r = 0.f, sy = 0.f;
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      const double y =
-          fmax(__builtin_fma(static_cast<double>(x[k]), c2, -mc), -256.0);
-      const float e = exp2_split(y);
-      r += e;
-      sy = __builtin_fmaf(-static_cast<float>(y), e, sy);
-    }
-    st.R += r;
-    st.S += sy;
-    return;
-  }
   if (bm > st.m) {
     shift_state(st, bm, c2);
     st.m = bm;
@@ -125,22 +124,22 @@ __device__ __forceinline__ void push_block(State& st, const float (&x)[N],
     for (int k = N - 1; k >= 0; --k) t = (x[k] == bm) ? idx[k] : t;
     st.tok = t;
   }
-  const double mc2 = static_cast<double>(st.m) * c2;
+  const double mc = static_cast<double>(st.m) * c2;
   float r = 0.f, sy = 0.f;
+  int ties = 0;
 #pragma unroll
   for (int k = 0; k < N; ++k) {
-    if (x[k] == st.m) {
-      st.ties += 1;
-    } else {
-      const double y =
-          fmax(__builtin_fma(static_cast<double>(x[k]), c2, -mc2), -256.0);
-      const float e = exp2_split(y);
-      r += e;
-      sy = __builtin_fmaf(-static_cast<float>(y), e, sy);
-    }
+    float yh;
+    float e = exp2_term(x[k], c2, mc, yh);
+    const bool is_max = x[k] == st.m;
+    e = is_max ? 0.f : e;
+    ties += is_max ? 1 : 0;
+    r += e;
+    sy = __builtin_fmaf(-yh, e, sy);
   }
   st.R += r;
   st.S += sy;
+  st.ties += ties;
 }
 
 // Reduce the block's states into thread 0's.
@@ -199,22 +198,43 @@ __global__ __launch_bounds__(kThreads) void score_kernel(ScoreArgs a) {
   constexpr int kStep = kThreads * kBlk;       // logits per workgroup step
   int v = v0;
   if (kVec) {
-    for (; v + kStep <= v1; v += kStep) {
+    // full steps, loads one step ahead of the arithmetic (the prefetch of
+    // the last step re-reads it, so every load is unconditional and in
+    // bounds and the wait before each step leaves the next one in flight)
+    const int nsteps = (v1 - v0) / kStep;
+    auto load = [&](int s, floatx4_t (&q)[kBlk / 4]) {
+      const int vs = v0 + s * kStep;
+#pragma unroll
+      for (int g = 0; g < kBlk / 4; ++g)
+        q[g] = __builtin_nontemporal_load(reinterpret_cast<const floatx4_t*>(
+            x + vs + (g * kThreads + threadIdx.x) * 4));
+    };
+    auto consume = [&](int s, const floatx4_t (&q)[kBlk / 4]) {
+      const int vs = v0 + s * kStep;
       float xs[kBlk];
       int idx[kBlk];
 #pragma unroll
-      for (int g = 0; g < kBlk / 4; ++g) {
-        const int vg = v + (g * kThreads + threadIdx.x) * 4;
-        const floatx4_t q = __builtin_nontemporal_load(
-            reinterpret_cast<const floatx4_t*>(x + vg));
+      for (int g = 0; g < kBlk / 4; ++g)
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          xs[g * 4 + k] = q[k];
-          idx[g * 4 + k] = vg + k;
+          xs[g * 4 + k] = q[g][k];
+          idx[g * 4 + k] = vs + (g * kThreads + threadIdx.x) * 4 + k;
         }
-      }
       push_block(st, xs, idx, a.c2);
+    };
+    if (nsteps > 0) {
+      floatx4_t qa[kBlk / 4], qb[kBlk / 4];
+      load(0, qa);
+      int s = 0;
+      for (; s + 2 <= nsteps; s += 2) {
+        load(min(s + 1, nsteps - 1), qb);
+        consume(s, qa);
+        load(min(s + 2, nsteps - 1), qa);
+        consume(s + 1, qb);
+      }
+      if (s < nsteps) consume(s, qa);
     }
+    v = v0 + nsteps * kStep;
   }
   // remainder (and the whole chunk without 16-byte alignment): one logit at
   // a time in increasing index order per thread
@@ -246,9 +266,12 @@ __global__ __launch_bounds__(kWave) void score_merge_kernel(ScoreArgs a) {
 }
 
 int plan_chunks(int B, int W, int V, int* chunk) {
-  // aim for >= 2048 workgroups over the B*W rows, chunks >= 16K elements
+  // about 768 workgroups over the B*W rows and at least two chunks per
+  // row, each chunk >= 16K elements: long enough that the per-workgroup
+  // merge is a small share, short enough that loads stay in flight
   const int rows = B * W;
-  int nchunk = (2048 + rows - 1) / rows;
+  int nchunk = (768 + rows - 1) / rows;
+  if (nchunk < 2) nchunk = 2;
   const int max_by_size = (V + 16383) / 16384;
   if (nchunk > max_by_size) nchunk = max_by_size;
   if (nchunk < 1) nchunk = 1;

@@ -135,3 +135,40 @@ def test_secondary_readings(lam, temp):
     for name in ("tiny", "qwen3_8b_layer"):
         wl = WL.WORKLOADS[name].replace(lam=lam, temp=temp)
         _full_check(wl, WL.step_inputs(wl, seed=3))
+
+
+def test_attention_workspace_reuse():
+    """One workspace, three calls with shrinking prefixes (so the number of
+    prefix splits per sequence changes between calls): the split arrival
+    counters must come back to zero after each call."""
+    import torch
+    from oracle import wedlm_oracle as O
+    from paper_2512_22737_amd import wedlm
+    wl = WL.Workload("reuse", 62, B=3, W=24, Hq=8, Hkv=2, D=128, V=300,
+                     prefix=2000, prefix_hi=6000, obs_frac=0.3,
+                     obs_frac_hi=0.6, spike=9.0)
+    d = WL.step_inputs(wl, seed=0)
+    dev = PL.to_dev(d)
+    c_full = d["win_start"].copy()
+    step = wedlm.DecodeStep(wl.B, wl.W, wl.Hq, wl.Hkv, wl.D, wl.V,
+                            int(c_full.max()))
+    for frac in (1.0, 0.5, 0.1):
+        c = (c_full * frac).astype(np.int32)
+        c_dev = torch.from_numpy(c).cuda()
+        step.reorder(dev["win_tok"], c_dev, dev["qkv_in"])
+        step.attn(dev["k_cache"], dev["v_cache"], dev["block_table"], c_dev)
+        got = step.out.float().cpu().numpy().astype(np.float64)
+        assert (step.attn_status.cpu().numpy() == 0).all()
+        for b in range(wl.B):
+            perm, pos, _, _ = O.reorder(list(d["win_tok"][b]), int(c[b]))
+            q, k, v = O.rope_window(d["qkv_in"][b], perm, pos, wl.Hq, wl.Hkv,
+                                    wl.theta)
+            kp, vp = WL.gather_prefix(d["k_cache"], d["v_cache"],
+                                      d["block_table"], b, int(c[b]))
+            ref, _ = O.window_attn(q, k, v, O.bf16_to_f64(kp),
+                                   O.bf16_to_f64(vp))
+            err = np.abs(got[b] - ref)
+            rel = np.linalg.norm(got[b] - ref) / np.linalg.norm(ref)
+            PL.log(f"  reuse frac {frac} seq {b} c={int(c[b])}: max abs "
+                   f"{err.max():.2e} rel {rel:.2e}")
+            assert err.max() <= PL.ATTN_MAX_ABS and rel <= PL.ATTN_REL_NORM
