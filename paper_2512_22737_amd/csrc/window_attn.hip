@@ -18,7 +18,7 @@
 //   QB MFMAs.  The transposed V page layout makes V^T rows contiguous.
 // Latency hiding: global loads run PF tiles ahead into a ring of register
 //   stages (tile t lives in stage t % PF), so about PF * 16 KB are in flight
-//   per workgroup; the LDS tile is double-buffered, one barrier per tile.
+//   per workgroup; LDS holds a ring of six tiles, one barrier per two.
 // Softmax: log2 domain, running max raised only when a tile's max exceeds
 //   it by more than 8 (p <= 2^8 otherwise), so the O rescale is rare.
 // Split-K: the prefix is split so that the grid fills the CUs; partials
@@ -172,6 +172,8 @@ struct Tile {
   }
 };
 
+constexpr int gcd_c(int x, int y) { return y == 0 ? x : gcd_c(y, x % y); }
+
 // Key row of the score tile held in MFMA output row m: bits 2 and 3 of m
 // swapped, so that output element e of a lane (hf = lane / 32) is key
 // 16*(e/8) + 8*hf + e%8 and each lane's slice of P^T is 8 contiguous keys.
@@ -185,7 +187,8 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   constexpr int NK = D / 16;          // k-steps of the score MFMA
   constexpr int NM = D / 32;          // 32-row blocks of O^T
   static_assert(PF >= 2, "register prefetch depth");
-  __shared__ __attribute__((aligned(1024))) char smem[3 * T::bytes];
+  constexpr int NS = 6;               // LDS ring of 32-key tile slots
+  __shared__ __attribute__((aligned(1024))) char smem[NS * T::bytes];
 
   int wg = blockIdx.x;
   const int split = wg % a.nsplit;
@@ -245,13 +248,15 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   // global loads of full prefix tile t into a register stage; page ids go
   // through the scalar cache, an invalid id is clamped to page 0 (in
   // bounds; the sequence's status records it)
+  const int np32 = a.num_pages > 0x7fffffff ? 0x7fffffff
+                                            : static_cast<int>(a.num_pages);
   auto fetch = [&](int t, u16x8_t (&r)[CPT]) {
     const int p0 = k0 + t * kTileKeys;
     int pg[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       int id = load_uniform(btb, p0 / kPage + h);
-      if (!(id >= 0 && id < a.num_pages)) { pages_ok = false; id = 0; }
+      if (!(id >= 0 && id < np32)) { pages_ok = false; id = 0; }
       pg[h] = id;
     }
 #pragma unroll
@@ -349,9 +354,15 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
           sc[q][e] = key <= lim ? sc[q][e] : kNegInf;
         }
       }
-      float mx = fmaxf(sc[q][0], sc[q][1]);
+      // three-input max tree: 16 scores in 8 v_max3
+      float t[6];
 #pragma unroll
-      for (int e = 2; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sc[q][e], sc[q][e + 1]));
+      for (int g = 0; g < 5; ++g)
+        t[g] = fmaxf(sc[q][3 * g], fmaxf(sc[q][3 * g + 1], sc[q][3 * g + 2]));
+      t[5] = sc[q][15];
+      float mx = fmaxf(t[0], fmaxf(t[1], t[2]));
+      mx = fmaxf(mx, fmaxf(t[3], t[4]));
+      mx = fmaxf(mx, t[5]);
       {
         float x0, x1;
         xor32_pair(mx, x0, x1);
@@ -383,15 +394,15 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e)
         pe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[q][e], a.scale_log2, -mc[q]));
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[q][h2][e] = static_cast<__bf16>(pe[h2 * 8 + e]);
       float ps[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g)
         ps[g] = (pe[4 * g] + pe[4 * g + 1]) + (pe[4 * g + 2] + pe[4 * g + 3]);
       l_run[q] += (ps[0] + ps[1]) + (ps[2] + ps[3]);
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pf[q][h2][e] = static_cast<__bf16>(pe[h2 * 8 + e]);
     }
   };
   auto softmax = [&](floatx16_t (&sc)[QB], bool need_mask, int base,
@@ -422,11 +433,15 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
                                                             o[q][m], 0, 0, 0);
   };
 
-  // ---- full prefix tiles.  LDS holds tiles t and t+1 (3-stage ring);
-  // tiles t+2 .. t+PF+1 are in flight in PF register stages.  Iteration t
-  // runs the score MFMAs of tile t+1, the softmax of tile t (VALU, under
-  // those MFMAs) and its P.V MFMAs, then moves tile t+2 from registers to
-  // LDS, refills that register stage with tile t+2+PF, and synchronises.
+  // ---- full prefix tiles.  Tile t lives in LDS slot t % 6; tiles
+  // t+4 .. t+3+PF are in flight in PF register stages.  Iteration t runs
+  // the score MFMAs of tile t+1, the softmax of tile t (VALU, under those
+  // MFMAs) and its P.V MFMAs, then moves tile t+3 from registers to LDS
+  // and refills that register stage with tile t+3+PF.  The workgroup
+  // synchronises after odd iterations only: a tile is written three
+  // iterations before its first read, so a barrier always lies between;
+  // a slot is rewritten only after two or more iterations that end in a
+  // barrier; and no slot being written is read in the same window.
   const bool partial_last = n_pre > 0 && (k1 - k0) % kTileKeys != 0;
   const int n_full = n_pre - (partial_last ? 1 : 0);
   u16x8_t rs[PF][CPT];
@@ -439,16 +454,18 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   if (n_full > 0) {
 #pragma unroll
     for (int j = 0; j < PF; ++j) fetch(min(j, last_full), rs[j]);
-    stash(rs[0], smem);
-    fetch(min(PF, last_full), rs[0]);
-    stash(rs[1 % PF], smem + T::bytes);
-    fetch(min(PF + 1, last_full), rs[1 % PF]);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      stash(rs[j % PF], smem + j * T::bytes);
+      fetch(min(j + PF, last_full), rs[j % PF]);
+    }
     __syncthreads();
     qk(smem, sbuf[0]);
   }
   {
   // unroll so register stages, LDS stages and score buffers are static
-  constexpr int U = (PF % 2 == 0 ? PF : 2 * PF) * (PF % 3 == 0 ? 1 : 3);
+  constexpr int U = PF * NS / gcd_c(PF, NS);
+  static_assert(U % 2 == 0, "iteration parity must be static");
   for (int t0 = 0; t0 < n_full; t0 += U) {
 #pragma unroll
     for (int j = 0; j < U; ++j) {
@@ -456,7 +473,7 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
       if (t >= n_full) break;
       // K fragments of tile t+1 (past the last full tile the stage holds a
       // re-read tile; that score block is never used)
-      const char* sk = smem + ((j + 1) % 3) * T::bytes;
+      const char* sk = smem + ((j + 1) % NS) * T::bytes;
       bf16x8_t kf[NK];
 #pragma unroll
       for (int kk = 0; kk < NK; ++kk)
@@ -464,7 +481,7 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
             bf16x8_t,
             *reinterpret_cast<const u16x8_t*>(sk + T::k_off(krow, 2 * kk + hf)));
       bf16x8_t vf[2][NM];
-      vread(smem + (j % 3) * T::bytes, vf);
+      vread(smem + (j % NS) * T::bytes, vf);
       float mc[QB];
       softmax_max(sbuf[j & 1], false, 0, 0, false, mc);
       // one scheduling region: the score MFMAs of tile t+1 interleaved with
@@ -486,9 +503,9 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
         __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // six VALU
       }
       pv(vf, pf);
-      stash(rs[(j + 2) % PF], smem + ((j + 2) % 3) * T::bytes);
-      fetch(min(t + 2 + PF, last_full), rs[(j + 2) % PF]);
-      __syncthreads();
+      stash(rs[(j + 3) % PF], smem + ((j + 3) % NS) * T::bytes);
+      fetch(min(t + 3 + PF, last_full), rs[(j + 3) % PF]);
+      if (j & 1) __syncthreads();
     }
   }
   }
@@ -501,7 +518,7 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   const int n_tail = (partial_last ? 1 : 0) + n_win;
   for (int tt = 0; tt < n_tail; ++tt) {
     const bool is_win = !(partial_last && tt == 0);
-    char* sb = smem + ((n_full + tt) % 3) * T::bytes;
+    char* sb = smem + ((n_full + tt) % NS) * T::bytes;
     int base, lim = 0;
     if (!is_win) {
       base = k0 + n_full * kTileKeys;
@@ -623,41 +640,73 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   }
 }
 
-// Merge of the split partials: one workgroup per (b, kv head, row), one
-// thread per d.
+// Merge of the split partials: D/4 threads per (b, kv head, row), each
+// owning four consecutive d, 256 threads per workgroup.  The (m, l) pairs
+// and up to eight partial vectors are loaded before any is used, so one
+// memory round trip covers the row.
+constexpr int kCombineThreads = 256;
+
 template <int D>
-__global__ __launch_bounds__(D) void attn_combine_kernel(AttnArgs a) {
-  int wg = blockIdx.x;
+__global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs a) {
+  constexpr int TPR = D / 4;                       // threads per row
+  constexpr int RPW = kCombineThreads / TPR;       // rows per workgroup
+  constexpr int kMaxFast = 8;
   const int rows = a.W * a.G;
-  const int r = wg % rows;
-  wg /= rows;
-  const int kvh = wg % a.Hkv;
-  const int b = wg / a.Hkv;
+  const int64_t gr = static_cast<int64_t>(blockIdx.x) * RPW + threadIdx.x / TPR;
+  if (gr >= static_cast<int64_t>(a.B) * a.Hkv * rows) return;
+  const int r = static_cast<int>(gr % rows);
+  const int bk = static_cast<int>(gr / rows);
+  const int kvh = bk % a.Hkv;
+  const int b = bk / a.Hkv;
   int c;
   if (!seq_ok(a, b, c)) return;
   const int nsplit_b = c > 0 ? (c + a.split_len - 1) / a.split_len : 1;
+  const int d = (threadIdx.x % TPR) * 4;
   const int64_t rows_base =
       (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
   const float2* ml = a.ws_ml + rows_base * a.nsplit;
-  float M = kNegInf;
-  for (int s = 0; s < nsplit_b; ++s) M = fmaxf(M, ml[s].x);
-  const float Mu = (M == kNegInf) ? 0.f : M;
-  float L = 0.f, acc = 0.f;
-  const int d = threadIdx.x;
   const float* op = a.ws_o + rows_base * a.nsplit * D + d;
-  for (int s = 0; s < nsplit_b; ++s) {
+  float2 mls[kMaxFast];
+  floatx4_t vs[kMaxFast];
+#pragma unroll
+  for (int s = 0; s < kMaxFast; ++s) {
+    if (s < nsplit_b) {
+      mls[s] = ml[s];
+      vs[s] = *reinterpret_cast<const floatx4_t*>(op + static_cast<int64_t>(s) * D);
+    }
+  }
+  float M = kNegInf;
+#pragma unroll
+  for (int s = 0; s < kMaxFast; ++s)
+    if (s < nsplit_b) M = fmaxf(M, mls[s].x);
+  for (int s = kMaxFast; s < nsplit_b; ++s) M = fmaxf(M, ml[s].x);
+  const float Mu = (M == kNegInf) ? 0.f : M;
+  float L = 0.f;
+  floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < kMaxFast; ++s) {
+    if (s < nsplit_b) {
+      const float w = __builtin_amdgcn_exp2f(mls[s].x - Mu);
+      L += w * mls[s].y;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[k] += w * vs[s][k];
+    }
+  }
+  for (int s = kMaxFast; s < nsplit_b; ++s) {
     const float w = __builtin_amdgcn_exp2f(ml[s].x - Mu);
     L += w * ml[s].y;
-    acc += w * op[static_cast<int64_t>(s) * D];
+    const floatx4_t v = *reinterpret_cast<const floatx4_t*>(op + static_cast<int64_t>(s) * D);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc[k] += w * v[k];
   }
   const int qi = r / a.G;
   const int qh = kvh * a.G + r % a.G;
+  const int64_t orow = (static_cast<int64_t>(b) * a.W + qi) * a.Hq + qh;
   const float inv = L > 0.f ? 1.f / L : 0.f;
-  a.out[((static_cast<int64_t>(b) * a.W + qi) * a.Hq + qh) * D + d] =
-      f32_to_bf16(acc * inv);
-  if (a.lse && d == 0)
-    a.lse[(static_cast<int64_t>(b) * a.W + qi) * a.Hq + qh] =
-        (M + __log2f(L)) * kLn2;
+  const u16x4_t o4 = {f32_to_bf16(acc[0] * inv), f32_to_bf16(acc[1] * inv),
+                      f32_to_bf16(acc[2] * inv), f32_to_bf16(acc[3] * inv)};
+  *reinterpret_cast<u16x4_t*>(a.out + orow * D + d) = o4;
+  if (a.lse && d == 0) a.lse[orow] = (M + __log2f(L)) * kLn2;
 }
 
 template <int D>
@@ -683,8 +732,11 @@ int launch(const AttnArgs& a, const Plan& p, hipStream_t st) {
   }
   WEDLM_LAUNCH_CHECK();
   if (a.nsplit > 1) {
-    hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(a.B * a.Hkv * a.W * a.G),
-                       dim3(D), 0, st, a);
+    const int64_t total_rows = static_cast<int64_t>(a.B) * a.Hkv * a.W * a.G;
+    constexpr int rpw = kCombineThreads / (D / 4);
+    hipLaunchKernelGGL((attn_combine_kernel<D>),
+                       dim3(static_cast<unsigned>((total_rows + rpw - 1) / rpw)),
+                       dim3(kCombineThreads), 0, st, a);
     WEDLM_LAUNCH_CHECK();
   }
   return WEDLM_OK;
