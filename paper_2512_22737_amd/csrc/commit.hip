@@ -13,7 +13,8 @@
 //               on ties, when nothing passes and a mask exists;
 //   the new window is the filled window shifted left by n, masks appended.
 // Then every thread of the workgroup copies the n committed K and V rows
-// into their cache slots (V transposed, per the page layout).
+// into their cache slots (V transposed, per the page layout), 16 bytes of
+// one row and head at a time.
 #include "common.h"
 
 using namespace wedlm;
@@ -146,23 +147,45 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
   __syncthreads();
   if (!s_ok) return;
 
-  // KV extend: physical rows 0..n-1 -> positions c..c+n-1
+  // KV extend: physical rows 0..n-1 -> positions c..c+n-1, 16-byte pieces
+  // of D/8 bf16 values.  K rows are contiguous in both layouts.  For V the
+  // lanes run over consecutive rows of one (head, 8 values of d), so the
+  // transposed stores of one page land in contiguous 32-byte rows.
   const int n = s_n, c = s_c;
   const int D = a.D, Hkv = a.Hkv;
+  const int DG = D / 8;
   const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
-  const int per_row = Hkv * D;
-  const int total = n * per_row;
+  const int total = n * Hkv * DG;
   for (int e = threadIdx.x; e < total; e += kThreads) {
-    const int j = e / per_row;
-    const int rem = e - j * per_row;
-    const int h = rem / D;
-    const int d = rem - h * D;
-    const int p = c + j;
-    const int64_t pg = bt[p / kPage];
-    const int row = p % kPage;
-    const int64_t src = ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + d;
-    a.k_cache[((pg * Hkv + h) * kPage + row) * D + d] = a.k_phys[src];
-    a.v_cache[((pg * Hkv + h) * D + d) * kPage + row] = a.v_phys[src];
+    // K: e = (j, h, dg), dg fastest
+    {
+      const int dg = e % DG;
+      const int jh = e / DG;
+      const int h = jh % Hkv;
+      const int j = jh / Hkv;
+      const int p = c + j;
+      const int64_t pg = bt[p / kPage];
+      const int row = p % kPage;
+      const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
+          a.k_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
+      *reinterpret_cast<u16x8_t*>(
+          a.k_cache + ((pg * Hkv + h) * kPage + row) * D + dg * 8) = v;
+    }
+    // V: e = (h, dg, j), j fastest
+    {
+      const int j = e % n;
+      const int hd = e / n;
+      const int dg = hd % DG;
+      const int h = hd / DG;
+      const int p = c + j;
+      const int64_t pg = bt[p / kPage];
+      const int row = p % kPage;
+      const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
+          a.v_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
+      uint16_t* dst = a.v_cache + ((pg * Hkv + h) * D + dg * 8) * kPage + row;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) dst[k * kPage] = v[k];
+    }
   }
 }
 

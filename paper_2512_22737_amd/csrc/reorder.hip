@@ -4,8 +4,8 @@
 // stable partition of the window from two ballots: physical row i < n_obs
 // takes the i-th filled slot, row i >= n_obs the (i - n_obs)-th mask slot.
 // The row's angles are computed once in fp64 and shared through LDS; every
-// query and key head of the row is rotated in fp64 and rounded to bf16, the
-// value heads are copied.  The kernel moves (Hq + 2 Hkv) * D * 2 bytes in and
+// query and key head of the row is rotated in fp64 and rounded to bf16 (16
+// bytes per load and store), the value heads are copied.  The kernel moves (Hq + 2 Hkv) * D * 2 bytes in and
 // out per row; it is HBM-bound and small next to attention and scoring.
 #include "common.h"
 
@@ -52,6 +52,21 @@ __global__ __launch_bounds__(kThreads) void reorder_rope_kernel(
   __syncthreads();
   const int src = s_src;
   const int half = D / 2;
+  const int H = Hq + 2 * Hkv;
+  const uint16_t* x = qkv_in + (static_cast<int64_t>(b) * W + src) * H * D;
+  // one item = 8 consecutive rotation pairs of one query or key head (two
+  // 16-byte loads, two 16-byte stores); the first round's loads go out
+  // before the angles are computed, so their latency hides under the fp64
+  // pow and sincos
+  const int chunks = half / 8;                     // items per head
+  const int n_items = (Hq + Hkv) * chunks;
+  int it = threadIdx.x;
+  u16x8_t lo8 = {}, hi8 = {};
+  if (it < n_items) {
+    const int head = it / chunks, j0 = (it - head * chunks) * 8;
+    lo8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0);
+    hi8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0 + half);
+  }
   if (threadIdx.x < half) {
     const int j = threadIdx.x;
     const double pos = static_cast<double>(win_start[b]) + src;
@@ -62,31 +77,34 @@ __global__ __launch_bounds__(kThreads) void reorder_rope_kernel(
     s_sin[j] = sn;
   }
   __syncthreads();
-
-  const int H = Hq + 2 * Hkv;
-  const uint16_t* x = qkv_in + (static_cast<int64_t>(b) * W + src) * H * D;
-  // rotate the Hq query heads and Hkv key heads: one (head, pair) per item
-  const int n_pairs = (Hq + Hkv) * half;
-  for (int p = threadIdx.x; p < n_pairs; p += kThreads) {
-    const int head = p / half;
-    const int j = p - head * half;
-    const double a = bf16_to_f32(x[head * D + j]);
-    const double c2 = bf16_to_f32(x[head * D + j + half]);
-    const double cs = s_cos[j], sn = s_sin[j];
-    const float lo = static_cast<float>(a * cs - c2 * sn);
-    const float hi = static_cast<float>(c2 * cs + a * sn);
+  for (; it < n_items; it += kThreads) {
+    const int head = it / chunks, j0 = (it - head * chunks) * 8;
+    if (it != static_cast<int>(threadIdx.x)) {
+      lo8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0);
+      hi8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0 + half);
+    }
+    u16x8_t olo, ohi;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const double a = bf16_to_f32(lo8[e]);
+      const double c2 = bf16_to_f32(hi8[e]);
+      const double cs = s_cos[j0 + e], sn = s_sin[j0 + e];
+      olo[e] = f32_to_bf16(static_cast<float>(a * cs - c2 * sn));
+      ohi[e] = f32_to_bf16(static_cast<float>(c2 * cs + a * sn));
+    }
     uint16_t* dst =
         (head < Hq)
             ? q_phys + ((static_cast<int64_t>(b) * W + i) * Hq + head) * D
             : k_phys +
                   ((static_cast<int64_t>(b) * W + i) * Hkv + (head - Hq)) * D;
-    dst[j] = f32_to_bf16(lo);
-    dst[j + half] = f32_to_bf16(hi);
+    *reinterpret_cast<u16x8_t*>(dst + j0) = olo;
+    *reinterpret_cast<u16x8_t*>(dst + j0 + half) = ohi;
   }
-  // copy the value heads
-  const uint16_t* xv = x + (Hq + Hkv) * D;
-  uint16_t* dv = v_phys + (static_cast<int64_t>(b) * W + i) * Hkv * D;
-  for (int e = threadIdx.x; e < Hkv * D; e += kThreads) dv[e] = xv[e];
+  // copy the value heads, 16 bytes per thread
+  const u16x8_t* xv = reinterpret_cast<const u16x8_t*>(x + (Hq + Hkv) * D);
+  u16x8_t* dv = reinterpret_cast<u16x8_t*>(
+      v_phys + (static_cast<int64_t>(b) * W + i) * Hkv * D);
+  for (int e = threadIdx.x; e < Hkv * D / 8; e += kThreads) dv[e] = xv[e];
 }
 
 }  // namespace
