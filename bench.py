@@ -3,9 +3,9 @@
 
 A step is one pass of the whole hot path over one batch: wedlm_reorder,
 wedlm_window_attn, wedlm_score and wedlm_commit, on synthetic inputs that
-are already resident in HBM.  The window state (win_tok, win_start) is reset
-from a pristine device copy before every step, so every timed step does the
-configured workload's work (the reset copies are inside the timed region).
+are already resident in HBM.  Every step starts from the workload's own
+window state (a fresh device copy per step, made before the timed region),
+so every timed step does the configured workload's work.
 Small workloads rotate over several input sets so that no timed step finds
 its inputs in the 256 MB last-level cache.
 
@@ -173,22 +173,23 @@ def main():
 
     def run(t, ev=None):
         s = sets[t % n_sets]
-        s["win_tok"].copy_(s["win_tok_0"])
-        s["win_start"].copy_(s["win_start_0"])
-        step.reorder(s["win_tok"], s["win_start"], s["qkv_in"])
+        win_tok, win_start = states[t]
+        step.reorder(win_tok, win_start, s["qkv_in"])
         if ev is not None:
             ev[0].record()
-        step.attn(s["k_cache"], s["v_cache"], s["block_table"],
-                  s["win_start"])
+        step.attn(s["k_cache"], s["v_cache"], s["block_table"], win_start)
         if ev is not None:
             ev[1].record()
         step.score(s["logits"])
-        step.commit(s["win_tok"], s["win_start"], s["k_cache"],
-                    s["v_cache"], s["block_table"])
+        step.commit(win_tok, win_start, s["k_cache"], s["v_cache"],
+                    s["block_table"])
 
-    for s in sets:
-        s["win_tok_0"] = s["win_tok"].clone()
-        s["win_start_0"] = s["win_start"].clone()
+    # every step starts from the workload's own window: one fresh copy of
+    # the window state per step, made before the timed region (the commit
+    # rewrites the window and re-appends the same cache slots each step)
+    states = [(sets[t % n_sets]["win_tok"].clone(),
+               sets[t % n_sets]["win_start"].clone())
+              for t in range(total_steps)]
 
     for t in range(args.warmup):
         run(t)
