@@ -172,3 +172,47 @@ def test_attention_workspace_reuse():
             PL.log(f"  reuse frac {frac} seq {b} c={int(c[b])}: max abs "
                    f"{err.max():.2e} rel {rel:.2e}")
             assert err.max() <= PL.ATTN_MAX_ABS and rel <= PL.ATTN_REL_NORM
+
+
+def test_attention_status_bits():
+    """Device-side checks of wedlm_window_attn: a prefix longer than
+    max_prefix_len is reported (WEDLM_SEQ_BAD_LEN) and that sequence is
+    skipped; a page id outside the cache is reported (WEDLM_SEQ_BAD_PAGE)
+    and read as page 0 (in bounds).  The other sequences are unaffected."""
+    import torch
+    from oracle import wedlm_oracle as O
+    from paper_2512_22737_amd import wedlm
+    wl = WL.Workload("status", 63, B=3, W=16, Hq=8, Hkv=2, D=128, V=300,
+                     prefix=300, prefix_hi=700, obs_frac=0.4, spike=9.0)
+    d = WL.step_inputs(wl, seed=1)
+    dev = PL.to_dev(d)
+    c = d["win_start"].copy()
+    max_prefix = int(c.max())
+    step = wedlm.DecodeStep(wl.B, wl.W, wl.Hq, wl.Hkv, wl.D, wl.V, max_prefix)
+    bad_c = c.copy()
+    bad_c[1] = max_prefix + 17                        # longer than the bound
+    bt = d["block_table"].copy()
+    bt[2, 3] = -1                                     # a hole inside c[2]
+    assert c[2] > 4 * WL.PAGE
+    c_dev = torch.from_numpy(bad_c).cuda()
+    bt_dev = torch.from_numpy(bt).cuda()
+    step.reorder(dev["win_tok"], c_dev, dev["qkv_in"])
+    step.out.fill_(0)
+    step.attn_status.zero_()
+    step.attn(dev["k_cache"], dev["v_cache"], bt_dev, c_dev)
+    st = step.attn_status.cpu().numpy()
+    assert st[0] == 0
+    assert st[1] & wedlm.SEQ_BAD_LEN
+    assert st[2] & wedlm.SEQ_BAD_PAGE
+    out = step.out.float().cpu().numpy().astype(np.float64)
+    assert np.isfinite(out[2]).all()                  # page 0 read instead
+    b = 0
+    perm, pos, _, _ = O.reorder(list(d["win_tok"][b]), int(c[b]))
+    q, k, v = O.rope_window(d["qkv_in"][b], perm, pos, wl.Hq, wl.Hkv,
+                            wl.theta)
+    kp, vp = WL.gather_prefix(d["k_cache"], d["v_cache"], d["block_table"],
+                              b, int(c[b]))
+    ref, _ = O.window_attn(q, k, v, O.bf16_to_f64(kp), O.bf16_to_f64(vp))
+    err = np.abs(out[b] - ref)
+    assert err.max() <= PL.ATTN_MAX_ABS
+    assert np.linalg.norm(out[b] - ref) / np.linalg.norm(ref) <= PL.ATTN_REL_NORM
