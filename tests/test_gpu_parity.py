@@ -58,6 +58,10 @@ SMALL = [
     ("w64_d128_g4", 64, 8, 2, 128, (200, 700), (0.0, 0.75), 2048),
     ("w64_d64_g2", 64, 4, 2, 64, (0, 31), (0.5, 1.0), 333),
     ("w7_d128_g2_long", 7, 4, 2, 128, (3000, 9000), (0.0, 0.5), 4096),
+    # eight waves at D = 64 (256 query rows per kv head), and two query
+    # blocks per kv head at D = 64 (384 rows)
+    ("w64_d64_g4", 64, 8, 2, 64, (100, 900), (0.1, 0.6), 1500),
+    ("w48_d64_g8", 48, 16, 2, 64, (40, 600), (0.0, 0.5), 640),
 ]
 
 
