@@ -34,6 +34,10 @@ using namespace wedlm;
 namespace {
 
 constexpr int kTileKeys = 32;       // keys per LDS tile (two 16-token pages)
+// Page ids of one split's full tiles are staged in LDS, so the tile loop
+// issues no scalar-cache loads (whose out-of-order return would make every
+// wait on the LDS reads a full drain).  A split is at most this many pages.
+constexpr int kMaxSplitPages = 2048;
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 
@@ -89,6 +93,8 @@ Plan make_plan(int B, int W, int Hq, int Hkv, int D, int max_prefix) {
   const int max_split = tiles / 8 > 1 ? tiles / 8 : 1;  // >= 8 tiles each
   if (nsplit > max_split) nsplit = max_split;
   if (nsplit < 1) nsplit = 1;
+  const int min_split = (tiles + kMaxSplitPages / 2 - 1) / (kMaxSplitPages / 2);
+  if (nsplit < min_split) nsplit = min_split;
   int tiles_per = (tiles + nsplit - 1) / nsplit;
   if (tiles_per < 1) tiles_per = 1;
   p.split_len = tiles_per * kTileKeys;
@@ -128,8 +134,8 @@ __device__ __forceinline__ void xor32_pair(float x, float& a, float& b) {
   b = __uint_as_float(r[1]);
 }
 
-// Wave-uniform read of a block-table entry through the scalar cache: it
-// stays off the vector-memory counter that paces the LDS ring.
+// Wave-uniform read of a block-table entry through the scalar cache (the
+// boundary tiles only; the tile loop reads page ids staged in LDS).
 __device__ __forceinline__ int load_uniform(const int32_t* p, int idx) {
   idx = __builtin_amdgcn_readfirstlane(idx);
   return ((const_i32_t*)p)[idx];
@@ -149,9 +155,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 //       same chunk) hit 16 different slots.
 //   V^T [2 pages][D rows][32 bytes]: chunk c (8 keys) of row d sits in slot
 //       c ^ ((d >> 3) & 1); 16 lanes reading rows d..d+15 cover all banks.
-// Tiles arrive by global_load_lds_dwordx4 (1 KB per wave instruction, lane L
-// writes bytes 16L..16L+15), so each lane loads the chunk that belongs in
-// its slot.
+// Tiles arrive through register stages: each lane loads fixed 16-byte
+// chunks of the tile's four contiguous page blocks and writes each to its
+// swizzled slot with ds_write_b128.
 template <int D>
 struct Tile {
   static constexpr int kBytes = kTileKeys * D * 2;
@@ -189,6 +195,7 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   static_assert(PF >= 2, "register prefetch depth");
   constexpr int NS = 6;               // LDS ring of 32-key tile slots
   __shared__ __attribute__((aligned(1024))) char smem[NS * T::bytes];
+  __shared__ int32_t pg_lds[kMaxSplitPages];   // page ids of the full tiles
 
   int wg = blockIdx.x;
   const int split = wg % a.nsplit;
@@ -245,20 +252,16 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   const int32_t* btb = a.bt + static_cast<int64_t>(b) * a.max_pages;
   bool pages_ok = true;
   constexpr int kBlockBytes = kPage * D * 2;
-  // global loads of full prefix tile t into a register stage; page ids go
-  // through the scalar cache, an invalid id is clamped to page 0 (in
-  // bounds; the sequence's status records it)
   const int np32 = a.num_pages > 0x7fffffff ? 0x7fffffff
                                             : static_cast<int>(a.num_pages);
-  auto fetch = [&](int t, u16x8_t (&r)[CPT]) {
-    const int p0 = k0 + t * kTileKeys;
-    int pg[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      int id = load_uniform(btb, p0 / kPage + h);
-      if (!(id >= 0 && id < np32)) { pages_ok = false; id = 0; }
-      pg[h] = id;
-    }
+  // page ids of full prefix tile t (staged in LDS, already checked)
+  auto ids_of = [&](int t) {
+    return *reinterpret_cast<const int2*>(pg_lds + 2 * t);
+  };
+  // global loads of a full prefix tile into a register stage
+  auto fetch_ids = [&](int2 ids, u16x8_t (&r)[CPT]) {
+    const int pg[2] = {__builtin_amdgcn_readfirstlane(ids.x),
+                       __builtin_amdgcn_readfirstlane(ids.y)};
 #pragma unroll
     for (int u = 0; u < CPT; ++u) {
       const int blk = g_blk[u];
@@ -272,6 +275,7 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
           u16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, g_voff[u], 0, 0));
     }
   };
+  auto fetch = [&](int t, u16x8_t (&r)[CPT]) { fetch_ids(ids_of(t), r); };
   auto stash = [&](const u16x8_t (&r)[CPT], char* sb) {
 #pragma unroll
     for (int u = 0; u < CPT; ++u)
@@ -451,6 +455,17 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   // so the loads form one straight-line stream and every wait before a
   // stash lets the younger tiles stay in flight.
   const int last_full = n_full - 1;
+  // page ids of the full tiles into LDS; an invalid id is clamped to page 0
+  // (in bounds) and reported
+  for (int i = threadIdx.x; i < 2 * n_full; i += NT) {
+    int id = btb[k0 / kPage + i];
+    if (!(id >= 0 && id < np32)) {
+      if (a.status) atomicOr(a.status + b, WEDLM_SEQ_BAD_PAGE);
+      id = 0;
+    }
+    pg_lds[i] = id;
+  }
+  __syncthreads();
   if (n_full > 0) {
 #pragma unroll
     for (int j = 0; j < PF; ++j) fetch(min(j, last_full), rs[j]);
@@ -462,53 +477,78 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
     __syncthreads();
     qk(smem, sbuf[0]);
   }
+  // page ids of the next fetch, read one iteration ahead of their use
+  int2 nid = ids_of(min(3 + PF, max(last_full, 0)));
+  // Iteration t (j = t mod U, a compile-time constant after unrolling, so
+  // register stages, LDS slots and score buffers are static).  The body is
+  // one macro used twice below; written as a lambda instead, the compiler
+  // allocates registers differently and spills inside the main loop.
+#define WEDLM_TILE_ITER                                                   \
+    /* K fragments of tile t+1 (past the last full tile the stage holds a  */\
+    /* re-read tile; that score block is never used)                       */\
+    const char* sk = smem + ((j + 1) % NS) * T::bytes;                    \
+    bf16x8_t kf[NK];                                                      \
+    _Pragma("unroll")                                                     \
+    for (int kk = 0; kk < NK; ++kk)                                       \
+      kf[kk] = __builtin_bit_cast(                                        \
+          bf16x8_t,                                                       \
+          *reinterpret_cast<const u16x8_t*>(sk + T::k_off(krow, 2 * kk + hf)));\
+    bf16x8_t vf[2][NM];                                                   \
+    vread(smem + (j % NS) * T::bytes, vf);                                \
+    float mc[QB];                                                         \
+    softmax_max(sbuf[j & 1], false, 0, 0, false, mc);                     \
+    /* one scheduling region: the score MFMAs of tile t+1 interleaved with */\
+    /* the exponentials of tile t                                          */\
+    bf16x8_t pf[QB][2];                                                   \
+    _Pragma("unroll")                                                     \
+    for (int q = 0; q < QB; ++q) {                                        \
+      _Pragma("unroll")                                                   \
+      for (int e = 0; e < 16; ++e) sbuf[(j + 1) & 1][q][e] = 0.f;         \
+      _Pragma("unroll")                                                   \
+      for (int kk = 0; kk < NK; ++kk)                                     \
+        sbuf[(j + 1) & 1][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(   \
+            kf[kk], qf[q][kk], sbuf[(j + 1) & 1][q], 0, 0, 0);            \
+    }                                                                     \
+    softmax_exp(sbuf[j & 1], mc, pf);                                     \
+    _Pragma("unroll")                                                     \
+    for (int i = 0; i < NK * QB; ++i) {                                   \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   /* one MFMA  */\
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   /* six VALU  */\
+    }                                                                     \
+    pv(vf, pf);                                                           \
+    stash(rs[(j + 3) % PF], smem + ((j + 3) % NS) * T::bytes);            \
+    {                                                                     \
+      const int2 cur = nid;                                               \
+      nid = ids_of(min(t + 4 + PF, last_full));                           \
+      fetch_ids(cur, rs[(j + 3) % PF]);                                   \
+    }                                                                     \
+    if (j & 1) __syncthreads();
   {
-  // unroll so register stages, LDS stages and score buffers are static
   constexpr int U = PF * NS / gcd_c(PF, NS);
   static_assert(U % 2 == 0, "iteration parity must be static");
-  for (int t0 = 0; t0 < n_full; t0 += U) {
+  // whole groups of U tiles with no exit inside, so the loop carries the
+  // same in-flight loads around its back edge as it receives on entry and
+  // the compiler's waits stay partial; then the remaining tiles
+  const int ngroups = n_full / U;
+  for (int t0 = 0; t0 < ngroups * U; t0 += U) {
 #pragma unroll
     for (int j = 0; j < U; ++j) {
       const int t = t0 + j;
-      if (t >= n_full) break;
-      // K fragments of tile t+1 (past the last full tile the stage holds a
-      // re-read tile; that score block is never used)
-      const char* sk = smem + ((j + 1) % NS) * T::bytes;
-      bf16x8_t kf[NK];
+      WEDLM_TILE_ITER
+    }
+  }
+  {
+    const int t0 = ngroups * U;
 #pragma unroll
-      for (int kk = 0; kk < NK; ++kk)
-        kf[kk] = __builtin_bit_cast(
-            bf16x8_t,
-            *reinterpret_cast<const u16x8_t*>(sk + T::k_off(krow, 2 * kk + hf)));
-      bf16x8_t vf[2][NM];
-      vread(smem + (j % NS) * T::bytes, vf);
-      float mc[QB];
-      softmax_max(sbuf[j & 1], false, 0, 0, false, mc);
-      // one scheduling region: the score MFMAs of tile t+1 interleaved with
-      // the exponentials of tile t
-      bf16x8_t pf[QB][2];
-#pragma unroll
-      for (int q = 0; q < QB; ++q) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sbuf[(j + 1) & 1][q][e] = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < NK; ++kk)
-          sbuf[(j + 1) & 1][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              kf[kk], qf[q][kk], sbuf[(j + 1) & 1][q], 0, 0, 0);
-      }
-      softmax_exp(sbuf[j & 1], mc, pf);
-#pragma unroll
-      for (int i = 0; i < NK * QB; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // six VALU
-      }
-      pv(vf, pf);
-      stash(rs[(j + 3) % PF], smem + ((j + 3) % NS) * T::bytes);
-      fetch(min(t + 3 + PF, last_full), rs[(j + 3) % PF]);
-      if (j & 1) __syncthreads();
+    for (int j = 0; j < U; ++j) {
+      const int t = t0 + j;
+      if (t >= n_full) goto tiles_done;
+      WEDLM_TILE_ITER
     }
   }
   }
+#undef WEDLM_TILE_ITER
+tiles_done:
   wait_vmcnt<0>();   // surplus fetches retire before the tail reuses stages
 
   // ---- boundary tiles, one at a time, plain synchronous loads: the
