@@ -22,7 +22,10 @@ What it computes, following WeDLM (arXiv 2512.22737):
   score        Entropy of the predicted distribution at each mask slot
                (Sec. 5.2, the quantity inside Eq. (11)) plus the greedy token.
   commit       Algorithm 1 commit / SelectByEntropy / Sample / refill steps,
-               with the distance-adjusted entropy of Eq. (11).
+               with the distance-adjusted entropy of Eq. (11); also the two
+               decoding rules the paper compares against: block-wise
+               stop-and-wait commit (Fig. 3, Sec. 6.4) and one token per
+               step (Sec. 6.2).
   stream       Algorithm 1's loop over many steps.
 
 Readings where the paper is silent or loose (each is listed with its reason
@@ -44,6 +47,13 @@ in the design notes of the repository):
   * RoPE pairs dimension i with i + D/2 ("rotate half"), frequency
     theta^(-2i/D); positions are 0-based, the window starting at c.
   * Softmax scale 1/sqrt(D); query head h reads kv head h // (Hq/Hkv).
+  * Block-wise rule: the block is the W-slot window.  Selection is the same
+    as streaming, but nothing is committed while any slot of the block is a
+    mask; the step that sees the whole block filled commits all W slots and
+    the window refills with W masks (Fig. 3 "stop-and-wait", Sec. 6.4).
+  * One-token rule: exactly one mask per step, the one with the smallest
+    H_i + lambda * d_i (ties: leftmost), whatever tau; commit as in
+    streaming (Sec. 6.2's unified step-wise scheme).
 
 Numbers are fp64 throughout, computed from the bf16-decoded inputs.
 """
@@ -228,26 +238,39 @@ def slot_of(block_table_row: Sequence[int], pos: int) -> int:
     return int(block_table_row[pos // PAGE]) * PAGE + pos % PAGE
 
 
+RULES = ("stream", "block", "one")
+
+
 def commit(win_tok: Sequence[int], c: int, entropy_phys: Sequence[float],
            argmax_phys: Sequence[int], tau: float, lam: float,
-           block_table_row: Optional[Sequence[int]] = None):
+           block_table_row: Optional[Sequence[int]] = None,
+           rule: str = "stream"):
     """One commit/select/fill/refill step on one window (Algorithm 1).
 
     entropy_phys / argmax_phys are indexed by physical row (the reordered
     order in which the forward produced them).  The entropy used in the
     decision should already be in the precision of the caller's choice.
+    rule: "stream" (Algorithm 1), "block" (block-wise stop-and-wait commit
+    of the whole window, Fig. 3 / Sec. 6.4) or "one" (one token per step,
+    Sec. 6.2).
     Returns a dict with n, committed tokens, committed slots, the selection
-    (logical slot -> 1 threshold / 2 fallback), the new window and c.
+    (logical slot -> 1 threshold / 2 smallest adjusted entropy), the new
+    window and c.
     """
+    if rule not in RULES:
+        raise ValueError(f"unknown decoding rule {rule!r}")
     W = len(win_tok)
     win = [int(t) for t in win_tok]
     perm, _, _, n_obs = reorder(win, c)
     phys = {s: i for i, s in enumerate(perm)}
 
-    # commit: the leading run of filled slots, in logical order
+    # commit: the leading run of filled slots, in logical order; the block
+    # rule commits only a window with no mask left, all W slots at once
     n = 0
     while n < W and win[n] != MASK:
         n += 1
+    if rule == "block" and n < W:
+        n = 0
     committed = win[:n]
     slots = ([slot_of(block_table_row, c + j) for j in range(n)]
              if block_table_row is not None else [])
@@ -259,7 +282,7 @@ def commit(win_tok: Sequence[int], c: int, entropy_phys: Sequence[float],
         s0 = masks[0]
         for s in masks:
             d = s - s0
-            if float(entropy_phys[phys[s]]) < tau - lam * d:
+            if rule != "one" and float(entropy_phys[phys[s]]) < tau - lam * d:
                 selected[s] = 1
         if not any(selected):
             best, best_key = None, None
@@ -314,7 +337,8 @@ def stream(win0: np.ndarray, c0: np.ndarray, steps: int,
            prefix_kv: Optional[Callable[[int], tuple]] = None,
            attn_steps: Sequence[int] = (),
            logits_row: Optional[Callable[[int, int, int], np.ndarray]] = None,
-           progress: Optional[Callable[[int], None]] = None):
+           progress: Optional[Callable[[int], None]] = None,
+           rule: str = "stream"):
     """Algorithm 1's loop for a batch of independent sequences.
 
     inputs_for_step(t) returns {"qkv_in": [B,W,Hq+2Hkv,D] bf16 bits} and,
@@ -366,7 +390,7 @@ def stream(win0: np.ndarray, c0: np.ndarray, steps: int,
                        else inp["logits"][b, i])
                 tok[i], H[i], _ = score_row(row, temperature)
             r = commit(win[b], c[b], to_f32_decision(H), tok, tau, lam,
-                       block_table[b])
+                       block_table[b], rule=rule)
             toks[b] += r["committed"]
             slots[b] += r["slots"]
             n_hist[t, b] = r["n"]

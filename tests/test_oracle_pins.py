@@ -368,6 +368,38 @@ def test_commit_hand_worked_trace():
     assert y == g["y"] and ys == g["y_slots"]
 
 
+@pytest.mark.parametrize("rule", ["block", "one"])
+def test_commit_rules_hand_worked_traces(rule):
+    """Block-wise stop-and-wait (Fig. 3, Sec. 6.4) and one token per step
+    (Sec. 6.2), traced by hand from the same first step as the streaming
+    trace."""
+    g = _golden("commit_trace_rules.json")
+    tr = g["rules"][rule]
+    win, c = g["W"] * [-1], g["c0"]
+    y, ys = [], []
+    for st in tr["steps"]:
+        assert win == st["win"] and c == st["c"]
+        H = [np.nan if h is None else h for h in st["H"]]
+        tok = [-1 if t is None else t for t in st["tok"]]
+        r = O.commit(win, c, H, tok, g["tau"], g["lam"], g["block_table"],
+                     rule=rule)
+        assert r["n"] == st["n"]
+        assert r["committed"] == st["committed"]
+        assert r["slots"] == st["slots"]
+        assert r["selected"] == st["selected"]
+        assert r["win"] == st["win_after"]
+        assert r["c"] == st["c_after"]
+        y += r["committed"]
+        ys += r["slots"]
+        win, c = r["win"], r["c"]
+    assert y == tr["y"] and ys == tr["y_slots"]
+
+
+def test_unknown_rule_is_rejected():
+    with pytest.raises(ValueError):
+        O.commit([-1, -1], 0, [0.1, 0.1], [1, 2], 0.9, 0.1, rule="blocks")
+
+
 def test_threshold_boundary_is_strict():
     """lambda = 0.1, d = 9: tau - lambda*d is exactly 0.0 in fp64, so a slot
     with H = 0 at distance 9 does not pass the strict test of Eq. (11)."""
@@ -394,7 +426,7 @@ def test_fallback_ties_go_left():
     assert r["selected"][best] == 2 and sum(map(bool, r["selected"])) == 1
 
 
-def _const_stream(W, steps, H_value, tau, lam, c0=7):
+def _const_stream(W, steps, H_value, tau, lam, c0=7, rule="stream"):
     """Stream in which every masked row has the given entropy."""
     win, c = [-1] * W, c0
     ns, toks, fills = [], [], {}
@@ -402,7 +434,7 @@ def _const_stream(W, steps, H_value, tau, lam, c0=7):
         perm, _, _, n_obs = O.reorder(win, c)
         H = [H_value] * W
         tok = [1000 * t + i for i in range(W)]
-        r = O.commit(win, c, H, tok, tau, lam, list(range(100)))
+        r = O.commit(win, c, H, tok, tau, lam, list(range(100)), rule=rule)
         ns.append(r["n"])
         toks.append(r["committed"])
         win, c = r["win"], r["c"]
@@ -427,6 +459,42 @@ def test_fallback_only_regime_is_autoregressive():
     ns, toks, c = _const_stream(W, steps, 0.3, 0.0, 10.0)
     assert ns == [0] + [1] * (steps - 1)
     assert c == 7 + steps - 1
+
+
+def test_block_rule_closed_forms():
+    """Block-wise rule.  All masks pass: one step fills the block, the next
+    commits it, as in streaming (p_cache 1/2).  One fill per step (tau <= 0,
+    leftmost by a large lambda): a block takes W fill steps and one commit
+    step, so p_cache = W / ((W + 1) W) = 1 / (W + 1), against streaming's
+    (steps - 1) / (steps W) in the same regime."""
+    W, steps = 8, 10
+    ns, _, c = _const_stream(W, steps, 0.0, 0.5, 0.0, rule="block")
+    assert ns == [0, W] * (steps // 2)
+    W, blocks = 5, 4
+    steps = blocks * (W + 1)
+    ns, toks, c = _const_stream(W, steps, 0.3, 0.0, 10.0, rule="block")
+    assert ns == ([0] * W + [W]) * blocks
+    assert c == 7 + W * blocks
+    assert O.p_cache(np.array(ns)[:, None], W) == pytest.approx(1 / (W + 1))
+    ns_s, _, _ = _const_stream(W, steps, 0.3, 0.0, 10.0)
+    assert O.p_cache(np.array(ns_s)[:, None], W) == \
+        pytest.approx((steps - 1) / (steps * W))
+
+
+def test_one_token_rule_is_autoregressive_whatever_tau():
+    """One token per step: even when every mask would pass the threshold
+    (tau = 10), exactly one mask is filled per step; with equal entropies
+    and lambda > 0 it is the leftmost, so from the second step on one token
+    is committed per step."""
+    W, steps = 6, 12
+    for tau in (10.0, 0.9, -1.0):
+        ns, toks, c = _const_stream(W, steps, 0.3, tau, 0.1, rule="one")
+        assert ns == [0] + [1] * (steps - 1)
+        # the token committed at step t + 1 was filled at step t: physical
+        # row 0 at step 0 (all masks), row 1 (the leftmost mask, behind one
+        # filled slot) afterwards
+        assert [t[0] for t in toks[1:]] == \
+            [0] + [1000 * t + 1 for t in range(1, steps - 1)]
 
 
 def test_slot_formula():
