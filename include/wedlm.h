@@ -14,6 +14,10 @@
  *                      SelectByEntropy with the adjusted entropy of Eq. (11),
  *                      greedy Sample, refill (Algorithm 1)
  *
+ * wedlm_commit_rule is wedlm_commit under a chosen decoding rule: Algorithm
+ * 1's streaming rule, block-wise stop-and-wait (Fig. 3, Sec. 6.4) or one
+ * token per step (Sec. 6.2).
+ *
  * Conventions shared by every call
  * --------------------------------
  *  - All array pointers are DEVICE pointers into memory the caller owns
@@ -72,6 +76,11 @@ enum {
 #define WEDLM_SEQ_CAPACITY 1 /* a needed position has no page (table full)  */
 #define WEDLM_SEQ_BAD_PAGE 2 /* a block-table entry is outside the cache    */
 #define WEDLM_SEQ_BAD_LEN 4  /* prefix length < 0 or > max_prefix_len      */
+
+/* decoding rules of wedlm_commit_rule */
+#define WEDLM_RULE_STREAMING 0 /* Algorithm 1 (what wedlm_commit does)     */
+#define WEDLM_RULE_BLOCK 1     /* block-wise stop-and-wait commit          */
+#define WEDLM_RULE_ONE_TOKEN 2 /* one mask filled per step                 */
 
 /*
  * wedlm_reorder -- Topological reordering, Eq. (5) and Eq. (6), plus the
@@ -217,6 +226,36 @@ int wedlm_commit(int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
                  int32_t W, int32_t Hkv, int32_t D, int32_t* n_commit,
                  int32_t* committed_tok, int32_t* committed_slot,
                  uint8_t* selected, int32_t* status, void* stream);
+
+/*
+ * wedlm_commit_rule -- wedlm_commit under the decoding rule `rule`, for
+ * comparing Algorithm 1 with the rules the paper measures it against.
+ * Arguments, layouts, outputs and errors are those of wedlm_commit; `rule`
+ * changes steps 1 and 2 only:
+ *   WEDLM_RULE_STREAMING  exactly wedlm_commit (Algorithm 1).
+ *   WEDLM_RULE_BLOCK      block-wise decoding with stop-and-wait commit
+ *                         (Fig. 3; Sec. 6.4 and Fig. 4c): the block is the
+ *                         W-slot window.  n = W if no slot is a mask, else
+ *                         n = 0, so nothing is committed until the whole
+ *                         block is filled; then all W slots commit and the
+ *                         window refills with W masks.  Selection as in
+ *                         step 2 (d measured from the leftmost mask).
+ *   WEDLM_RULE_ONE_TOKEN  the unified step-wise scheme of Sec. 6.2: exactly
+ *                         one mask per step, the one with the smallest
+ *                         (double)H + lambda * d (ties: leftmost), whatever
+ *                         tau; selected = 2 for it.  Commit as in step 1.
+ * Any other rule value returns WEDLM_E_ARG.
+ */
+int wedlm_commit_rule(int32_t* win_tok, int32_t* win_start,
+                      const int32_t* argmax, const float* entropy, double tau,
+                      double lambda, const uint16_t* k_phys,
+                      const uint16_t* v_phys, uint16_t* k_cache,
+                      uint16_t* v_cache, int64_t num_pages,
+                      const int32_t* block_table, int32_t max_pages, int32_t B,
+                      int32_t W, int32_t Hkv, int32_t D, int32_t* n_commit,
+                      int32_t* committed_tok, int32_t* committed_slot,
+                      uint8_t* selected, int32_t* status, int32_t rule,
+                      void* stream);
 
 /* Message for a WEDLM_* return code (static storage). */
 const char* wedlm_strerror(int code);

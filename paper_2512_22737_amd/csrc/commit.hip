@@ -1,14 +1,20 @@
 // Algorithm 1 after the forward: commit the leftmost filled run, extend the
 // KV cache with its rows, SelectByEntropy with the distance-adjusted entropy
-// of Eq. (11), greedy Sample, and refill the window to W slots.
+// of Eq. (11), greedy Sample, and refill the window to W slots.  Two other
+// decoding rules share the kernel: block-wise stop-and-wait (Fig. 3,
+// Sec. 6.4: the window is the block and is committed only once no mask is
+// left, all W slots at once) and one token per step (Sec. 6.2: only the
+// smallest adjusted entropy is filled, whatever tau).
 //
 // One workgroup per sequence.  Wave 0 holds the window, one slot per lane:
 //   n         = count of trailing ones of the filled-slot ballot (the leading
 //               filled run in logical order; these are physical rows 0..n-1
-//               after the stable reordering);
+//               after the stable reordering); under the block rule W when no
+//               slot is a mask, else 0;
 //   phys(s)   = n_obs + rank of mask s among the masks (Eq. 5/6 inverse);
 //   select s  iff (double)H_phys(s) < tau - lambda*(s - s0), evaluated
-//               without contraction so it rounds like the scalar reference;
+//               without contraction so it rounds like the scalar reference
+//               (s0 = the leftmost mask; never under the one-token rule);
 //   fallback  = argmin over masks of (double)H + lambda*(s - s0), leftmost
 //               on ties, when nothing passes and a mask exists;
 //   the new window is the filled window shifted left by n, masks appended.
@@ -41,6 +47,7 @@ struct CommitArgs {
   int32_t* committed_slot;
   uint8_t* selected;
   int32_t* status;
+  int rule;               // WEDLM_RULE_*
 };
 
 #pragma clang fp contract(off)
@@ -65,7 +72,8 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
     const uint64_t maskb = ballot(is_mask);
     const uint64_t filledb = ballot(in && !is_mask);
     const int n_o = __popcll(filledb);
-    const int n = maskb ? __ffsll(static_cast<long long>(maskb)) - 1 : W;
+    const int s0 = maskb ? __ffsll(static_cast<long long>(maskb)) - 1 : W;
+    const int n = (a.rule == WEDLM_RULE_BLOCK) ? (maskb ? 0 : W) : s0;
     const int c = a.win_start[b];
     const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
 
@@ -99,7 +107,6 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
       }
     } else {
       // SelectByEntropy over the mask slots (Eq. 11)
-      const int s0 = n;  // the leftmost mask ends the leading filled run
       const int below = __popcll(maskb & ((s == 0) ? 0ull : (~0ull >> (64 - s))));
       const int phys = n_o + below;
       double h = 0.0;
@@ -109,7 +116,8 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
         tok = a.argmax[b * W + phys];
       }
       const int d = s - s0;
-      const bool pass = is_mask && h < threshold_of(a.tau, a.lam, d);
+      const bool pass = a.rule != WEDLM_RULE_ONE_TOKEN && is_mask &&
+                        h < threshold_of(a.tau, a.lam, d);
       const uint64_t passb = ballot(pass);
       bool fb = false;
       if (passb == 0 && maskb != 0) {
@@ -191,21 +199,25 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
 
 }  // namespace
 
-extern "C" int wedlm_commit(int32_t* win_tok, int32_t* win_start,
-                            const int32_t* argmax, const float* entropy,
-                            double tau, double lambda, const uint16_t* k_phys,
-                            const uint16_t* v_phys, uint16_t* k_cache,
-                            uint16_t* v_cache, int64_t num_pages,
-                            const int32_t* block_table, int32_t max_pages,
-                            int32_t B, int32_t W, int32_t Hkv, int32_t D,
-                            int32_t* n_commit, int32_t* committed_tok,
-                            int32_t* committed_slot, uint8_t* selected,
-                            int32_t* status, void* stream) {
+namespace {
+
+int commit_impl(int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
+                const float* entropy, double tau, double lambda,
+                const uint16_t* k_phys, const uint16_t* v_phys,
+                uint16_t* k_cache, uint16_t* v_cache, int64_t num_pages,
+                const int32_t* block_table, int32_t max_pages, int32_t B,
+                int32_t W, int32_t Hkv, int32_t D, int32_t* n_commit,
+                int32_t* committed_tok, int32_t* committed_slot,
+                uint8_t* selected, int32_t* status, int32_t rule,
+                void* stream) {
   if (!win_tok || !win_start || !argmax || !entropy || !k_phys || !v_phys ||
       !k_cache || !v_cache || !block_table || !n_commit || !committed_tok ||
       !committed_slot || !selected || !status)
     return WEDLM_E_ARG;
   if (tau != tau || lambda != lambda || num_pages < 1 || max_pages < 1)
+    return WEDLM_E_ARG;
+  if (rule != WEDLM_RULE_STREAMING && rule != WEDLM_RULE_BLOCK &&
+      rule != WEDLM_RULE_ONE_TOKEN)
     return WEDLM_E_ARG;
   if (B < 1 || B > (1 << 30) || W < 1 || W > WEDLM_MAX_WINDOW || Hkv < 1 ||
       (D != 64 && D != 128))
@@ -219,8 +231,42 @@ extern "C" int wedlm_commit(int32_t* win_tok, int32_t* win_start,
   a.W = W; a.Hkv = Hkv; a.D = D;
   a.n_commit = n_commit; a.committed_tok = committed_tok;
   a.committed_slot = committed_slot; a.selected = selected; a.status = status;
+  a.rule = rule;
   hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), a);
   WEDLM_LAUNCH_CHECK();
   return WEDLM_OK;
+}
+
+}  // namespace
+
+extern "C" int wedlm_commit(int32_t* win_tok, int32_t* win_start,
+                            const int32_t* argmax, const float* entropy,
+                            double tau, double lambda, const uint16_t* k_phys,
+                            const uint16_t* v_phys, uint16_t* k_cache,
+                            uint16_t* v_cache, int64_t num_pages,
+                            const int32_t* block_table, int32_t max_pages,
+                            int32_t B, int32_t W, int32_t Hkv, int32_t D,
+                            int32_t* n_commit, int32_t* committed_tok,
+                            int32_t* committed_slot, uint8_t* selected,
+                            int32_t* status, void* stream) {
+  return commit_impl(win_tok, win_start, argmax, entropy, tau, lambda, k_phys,
+                     v_phys, k_cache, v_cache, num_pages, block_table,
+                     max_pages, B, W, Hkv, D, n_commit, committed_tok,
+                     committed_slot, selected, status, WEDLM_RULE_STREAMING,
+                     stream);
+}
+
+extern "C" int wedlm_commit_rule(
+    int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
+    const float* entropy, double tau, double lambda, const uint16_t* k_phys,
+    const uint16_t* v_phys, uint16_t* k_cache, uint16_t* v_cache,
+    int64_t num_pages, const int32_t* block_table, int32_t max_pages,
+    int32_t B, int32_t W, int32_t Hkv, int32_t D, int32_t* n_commit,
+    int32_t* committed_tok, int32_t* committed_slot, uint8_t* selected,
+    int32_t* status, int32_t rule, void* stream) {
+  return commit_impl(win_tok, win_start, argmax, entropy, tau, lambda, k_phys,
+                     v_phys, k_cache, v_cache, num_pages, block_table,
+                     max_pages, B, W, Hkv, D, n_commit, committed_tok,
+                     committed_slot, selected, status, rule, stream);
 }

@@ -60,6 +60,10 @@ def _load():
     lib.wedlm_commit.argtypes = [P, P, P, P, D_, D_, P, P, P, P, I64, P, I32,
                                  I32, I32, I32, I32, P, P, P, P, P, P]
     lib.wedlm_commit.restype = ctypes.c_int
+    lib.wedlm_commit_rule.argtypes = [P, P, P, P, D_, D_, P, P, P, P, I64, P,
+                                      I32, I32, I32, I32, I32, P, P, P, P, P,
+                                      I32, P]
+    lib.wedlm_commit_rule.restype = ctypes.c_int
     lib.wedlm_strerror.argtypes = [ctypes.c_int]
     lib.wedlm_strerror.restype = ctypes.c_char_p
     lib.wedlm_version.argtypes = []
@@ -74,7 +78,12 @@ def lib():
 
 EXPORTED = ["wedlm_reorder", "wedlm_window_attn_workspace_size",
             "wedlm_window_attn", "wedlm_score_workspace_size", "wedlm_score",
-            "wedlm_commit", "wedlm_strerror", "wedlm_version"]
+            "wedlm_commit", "wedlm_commit_rule", "wedlm_strerror",
+            "wedlm_version"]
+
+# decoding rules of wedlm_commit_rule (include/wedlm.h)
+RULE_STREAMING, RULE_BLOCK, RULE_ONE_TOKEN = 0, 1, 2
+RULES = {"stream": RULE_STREAMING, "block": RULE_BLOCK, "one": RULE_ONE_TOKEN}
 
 
 def _check(code: int, what: str):
@@ -202,15 +211,15 @@ def wedlm_score(logits, n_obs, temperature: float, argmax, entropy,
     _check(code, "wedlm_score")
 
 
-def wedlm_commit(win_tok, win_start, argmax, entropy, tau: float, lam: float,
-                 k_phys, v_phys, k_cache, v_cache, block_table, n_commit,
-                 committed_tok, committed_slot, selected, status) -> None:
+def _commit_args(win_tok, win_start, argmax, entropy, tau, lam, k_phys,
+                 v_phys, k_cache, v_cache, block_table, n_commit,
+                 committed_tok, committed_slot, selected, status):
     B, W = win_tok.shape
     Hkv, D = k_phys.shape[2], k_phys.shape[3]
     P = k_cache.shape[0]
     maxp = block_table.shape[1]
     i32 = (torch.int32,)
-    code = _load().wedlm_commit(
+    return [
         _t(win_tok, "win_tok", i32, (B, W)), _t(win_start, "win_start", i32, (B,)),
         _t(argmax, "argmax", i32, (B, W)),
         _t(entropy, "entropy", (torch.float32,), (B, W)), float(tau),
@@ -223,8 +232,27 @@ def wedlm_commit(win_tok, win_start, argmax, entropy, tau: float, lam: float,
         _t(committed_tok, "committed_tok", i32, (B, W)),
         _t(committed_slot, "committed_slot", i32, (B, W)),
         _t(selected, "selected", (torch.uint8,), (B, W)),
-        _t(status, "status", i32, (B,)), _stream())
-    _check(code, "wedlm_commit")
+        _t(status, "status", i32, (B,))]
+
+
+def wedlm_commit(win_tok, win_start, argmax, entropy, tau: float, lam: float,
+                 k_phys, v_phys, k_cache, v_cache, block_table, n_commit,
+                 committed_tok, committed_slot, selected, status) -> None:
+    args = _commit_args(win_tok, win_start, argmax, entropy, tau, lam, k_phys,
+                        v_phys, k_cache, v_cache, block_table, n_commit,
+                        committed_tok, committed_slot, selected, status)
+    _check(_load().wedlm_commit(*args, _stream()), "wedlm_commit")
+
+
+def wedlm_commit_rule(win_tok, win_start, argmax, entropy, tau: float,
+                      lam: float, k_phys, v_phys, k_cache, v_cache,
+                      block_table, n_commit, committed_tok, committed_slot,
+                      selected, status, rule: int) -> None:
+    args = _commit_args(win_tok, win_start, argmax, entropy, tau, lam, k_phys,
+                        v_phys, k_cache, v_cache, block_table, n_commit,
+                        committed_tok, committed_slot, selected, status)
+    _check(_load().wedlm_commit_rule(*args, int(rule), _stream()),
+           "wedlm_commit_rule")
 
 
 class DecodeStep:
@@ -235,8 +263,10 @@ class DecodeStep:
     [B,W,V] fp32 (physical row order)."""
 
     def __init__(self, B, W, Hq, Hkv, D, V, max_prefix_len, theta=1e6,
-                 tau=0.9, lam=0.01, temperature=0.1, device="cuda"):
+                 tau=0.9, lam=0.01, temperature=0.1, device="cuda",
+                 rule="stream"):
         self.B, self.W, self.Hq, self.Hkv, self.D, self.V = B, W, Hq, Hkv, D, V
+        self.rule = RULES[rule]
         self.theta, self.tau, self.lam, self.temperature = (theta, tau, lam,
                                                             temperature)
         self.max_prefix_len = int(max_prefix_len)
@@ -292,10 +322,14 @@ class DecodeStep:
                     self.entropy, self.pmax, self.score_ws, V=self.V)
 
     def commit(self, win_tok, win_start, k_cache, v_cache, block_table):
-        wedlm_commit(win_tok, win_start, self.argmax, self.entropy, self.tau,
-                     self.lam, self.k_phys, self.v_phys, k_cache, v_cache,
-                     block_table, self.n_commit, self.committed_tok,
-                     self.committed_slot, self.selected, self.status)
+        args = (win_tok, win_start, self.argmax, self.entropy, self.tau,
+                self.lam, self.k_phys, self.v_phys, k_cache, v_cache,
+                block_table, self.n_commit, self.committed_tok,
+                self.committed_slot, self.selected, self.status)
+        if self.rule == RULE_STREAMING:
+            wedlm_commit(*args)
+        else:
+            wedlm_commit_rule(*args, self.rule)
 
     def __call__(self, win_tok, win_start, qkv_in, logits, k_cache, v_cache,
                  block_table):

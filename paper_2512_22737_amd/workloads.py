@@ -112,6 +112,7 @@ def rng_for(seed: int, cid: int, step: int, part: int) -> np.random.Generator:
 
 # parts of the seed key
 _P_PREFIX_LEN, _P_WINDOW, _P_QKV, _P_TABLE, _P_LOGITS, _P_POOL, _P_KV = range(7)
+_P_DECISION = 7
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -323,6 +324,24 @@ def step_inputs(wl: Workload, seed: int = 0, step: int = 0,
         d["logits"] = logits(wl, n_obs if nan_observed_rows else None, seed,
                              step)
     return d
+
+
+def decision_inputs(B: int, W: int, Hkv: int, D: int, seed: int, step: int,
+                    quantum: float = 0.0625, levels: int = 24,
+                    p_zero: float = 0.3):
+    """Synthetic per-physical-row inputs of the commit step alone: entropy
+    [B, W] fp32 on a grid of `quantum` (so equal values, and sums with a
+    binary lambda, are exact on every side), a share `p_zero` of rows at
+    entropy 0, argmax [B, W] int32 and window K/V rows [B, W, Hkv, D] bf16
+    bits.  Stream of steps keyed by `step`; cid 100 keeps it apart from the
+    workloads' own streams."""
+    rng = rng_for(seed, 100, step, _P_DECISION)
+    h = rng.integers(0, levels, size=(B, W)).astype(np.float64) * quantum
+    h[rng.random((B, W)) < p_zero] = 0.0
+    tok = rng.integers(0, 1 << 20, size=(B, W)).astype(np.int32)
+    k = _normal_bf16(rng, (B, W, Hkv, D))
+    v = _normal_bf16(rng, (B, W, Hkv, D))
+    return h.astype(np.float32), tok, k, v
 
 
 def gather_prefix(k_cache: np.ndarray, v_cache: np.ndarray, bt: np.ndarray,

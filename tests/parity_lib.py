@@ -42,9 +42,11 @@ def bf16_bits(t) -> np.ndarray:
     return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def run_gpu_step(wl: WL.Workload, d: dict, max_prefix: Optional[int] = None):
-    """One decode step through the C ABI.  Returns host copies of every
-    output plus the device state for further steps."""
+def run_gpu_step(wl: WL.Workload, d: dict, max_prefix: Optional[int] = None,
+                 rule: str = "stream"):
+    """One decode step through the C ABI (under the decoding rule `rule`).
+    Returns host copies of every output plus the device state for further
+    steps."""
     import torch
     from paper_2512_22737_amd import wedlm
     dev = to_dev(d)
@@ -52,7 +54,7 @@ def run_gpu_step(wl: WL.Workload, d: dict, max_prefix: Optional[int] = None):
     mp = int(c.max()) if max_prefix is None else max_prefix
     step = wedlm.DecodeStep(wl.B, wl.W, wl.Hq, wl.Hkv, wl.D, wl.V, mp,
                             theta=wl.theta, tau=wl.tau, lam=wl.lam,
-                            temperature=wl.temp)
+                            temperature=wl.temp, rule=rule)
     step(dev["win_tok"], dev["win_start"], dev["qkv_in"], dev["logits"],
          dev["k_cache"], dev["v_cache"], dev["block_table"])
     torch.cuda.synchronize()
@@ -77,7 +79,7 @@ def run_gpu_step(wl: WL.Workload, d: dict, max_prefix: Optional[int] = None):
 
 
 def oracle_step(wl: WL.Workload, d: dict, attn_seqs: Sequence[int] = (),
-                rows=None, heads=None):
+                rows=None, heads=None, rule: str = "stream"):
     """The oracle's view of the same step.  Attention is evaluated for the
     listed sequences (all rows/heads unless sampled)."""
     res = []
@@ -100,7 +102,7 @@ def oracle_step(wl: WL.Workload, d: dict, attn_seqs: Sequence[int] = (),
         tok, H, pm = O.score(d["logits"][b], n_obs, wl.temp)
         e.update(argmax=tok, entropy=H, pmax=pm)
         cm = O.commit(win, c, O.to_f32_decision(H), tok, wl.tau, wl.lam,
-                      d["block_table"][b])
+                      d["block_table"][b], rule=rule)
         e["commit"] = cm
         res.append(e)
     return res
