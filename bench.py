@@ -13,6 +13,14 @@ Prints ONE JSON line: window tokens/s (B*W per step time), the roofline of
 the dominant kernel (window attention: algorithmic bytes per launch over its
 HIP-event-timed average duration, against 8 TB/s), and the fp64 CPU oracle
 timed on a bounded sample of the same workload.
+
+--compare-rules instead runs the streaming workload (16 sequences, starting
+prefix 1024, W=32, V=151936, fresh synthetic logits every step) under each
+decoding rule of wedlm_commit_rule (Algorithm 1's streaming commit,
+block-wise stop-and-wait, one token per step) at several entropy thresholds,
+and prints one JSON line per run: p_cache (Eq. 4), committed tokens per
+step, steps to reach 128 committed tokens, and committed tokens per second
+of step time.
 """
 import argparse
 import hashlib
@@ -105,6 +113,82 @@ def cpu_baseline(wl, d, seed):
                        f"{len(os.sched_getaffinity(0))} cores")}
 
 
+def compare_rules(args, dev):
+    """Decoding rules on the streaming workload: every run starts from the
+    same all-mask windows at prefix 1024 and draws the same per-step logits
+    (they do not depend on the window state), so the rules differ only in
+    what they commit and fill.  Step time is the sum of HIP-event intervals
+    around the four calls of each step (input generation excluded)."""
+    import numpy as np
+    import torch
+    from paper_2512_22737_amd import wedlm
+    from paper_2512_22737_amd import workloads as WL
+    wl0 = WL.WORKLOADS["stream512"]
+    S = min(args.rule_steps, wl0.steps)
+    seed = args.seed
+    wl = wl0
+    print(f"# generating inputs for {wl.name}", file=sys.stderr, flush=True)
+    d = WL.step_inputs(wl, seed=seed, nan_observed_rows=False)
+
+    def up(a):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        if a.dtype == np.uint16:
+            t = t.view(torch.int16).view(torch.bfloat16)
+        return t.to(dev)
+
+    base = {k: up(v) for k, v in d.items() if isinstance(v, np.ndarray)}
+    # Q/K/V do not enter any decision: four sets, cycled
+    qkv_sets = [up(d["qkv_in"])] + [up(WL.qkv(wl, seed, t))
+                                    for t in range(1, 4)]
+    pool = torch.from_numpy(WL.logit_pool(wl, seed)).to(dev)
+    c0 = d["win_start"]
+    max_prefix = int(c0.max()) + S * wl.W
+    target = 128
+    runs = [(sp, tau, rule) for sp in (wl0.spike_prob, 0.5)
+            for tau in (0.3, 0.6, 0.9) for rule in ("stream", "block", "one")]
+    for spike_prob, tau, rule in runs:
+            # the share of confident (spiked) rows sets how fast masks resolve
+            wl = wl0.replace(spike_prob=spike_prob)
+            step = wedlm.DecodeStep(wl.B, wl.W, wl.Hq, wl.Hkv, wl.D, wl.V,
+                                    max_prefix, theta=wl.theta, tau=tau,
+                                    lam=wl.lam, temperature=wl.temp,
+                                    device=dev, rule=rule)
+            win_tok = base["win_tok"].clone()
+            win_start = base["win_start"].clone()
+            evs = [(torch.cuda.Event(enable_timing=True),
+                    torch.cuda.Event(enable_timing=True)) for _ in range(S)]
+            ns = []
+            for t in range(S):
+                logits = WL.logits_torch(wl, pool, seed, t)
+                evs[t][0].record()
+                step(win_tok, win_start, qkv_sets[t % 4], logits,
+                     base["k_cache"], base["v_cache"], base["block_table"])
+                evs[t][1].record()
+                ns.append(step.n_commit.clone())
+            torch.cuda.synchronize()
+            n = torch.stack(ns).cpu().numpy()            # [S, B]
+            st = int(step.status.abs().sum().item())
+            ms = sum(a.elapsed_time(b) for a, b in evs)
+            committed = int(n.sum())
+            cum = np.cumsum(n, axis=0)
+            reach = [int(np.argmax(cum[:, b] >= target)) + 1
+                     for b in range(wl.B) if cum[-1, b] >= target]
+            print(json.dumps({
+                "kind": "decoding_rule", "rule": rule, "tau": tau,
+                "lambda": wl.lam, "temperature": wl.temp,
+                "spiked_row_share": spike_prob,
+                "workload": wl.name, "B": wl.B, "W": wl.W,
+                "prefix_start": int(c0.min()), "steps": S,
+                "committed_tokens": committed,
+                "p_cache": committed / (S * wl.B * wl.W),
+                "tokens_per_step_per_seq": committed / (S * wl.B),
+                "steps_to_128_tokens": (float(np.mean(reach))
+                                        if len(reach) == wl.B else None),
+                "ms_per_step": ms / S,
+                "committed_tokens_per_s": committed / (ms / 1e3),
+                "status_nonzero": st}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,6 +197,10 @@ def main():
     ap.add_argument("--workload", default="long_prefix")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--compare-rules", action="store_true",
+                    help="p_cache and committed tokens/s of the decoding "
+                         "rules on the streaming workload, then exit")
+    ap.add_argument("--rule-steps", type=int, default=128)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for "
                          "scaling HBM counters) and exit")
@@ -140,6 +228,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "launches": 5}), flush=True)
+        return
+
+    if args.compare_rules:
+        compare_rules(args, dev)
         return
 
     wl = WL.WORKLOADS[args.workload]
