@@ -27,6 +27,9 @@ What it computes, following WeDLM (arXiv 2512.22737):
                stop-and-wait commit (Fig. 3, Sec. 6.4) and one token per
                step (Sec. 6.2).
   stream       Algorithm 1's loop over many steps.
+  lm_head_score  The logits of the forward's output layer (hidden states
+               times the vocabulary matrix) scored as above, for the fused
+               LM-head kernel.
 
 Readings where the paper is silent or loose (each is listed with its reason
 in the design notes of the repository):
@@ -197,16 +200,18 @@ def window_attn(q: np.ndarray, k_win: np.ndarray, v_win: np.ndarray,
 # Sec. 5.2: entropy of a mask slot's predicted distribution, greedy token
 # --------------------------------------------------------------------------
 
-def score_row(logit_row: np.ndarray, temperature: float):
+def score_row(logit_row: np.ndarray, temperature: float,
+              as_f32: bool = True):
     """Greedy token, entropy H (nats) and top probability of
     p = softmax(logits / T).
 
     H = -sum_v p_v log p_v, with log p_v = z_v - log Z written out so that
     nothing cancels: z_v = (l_v - l_max) / T and log Z = log1p(sum over
-    v != argmax of e^{z_v})."""
-    x32 = np.asarray(logit_row, dtype=np.float32)
-    tok = int(np.argmax(x32))                      # first maximum
-    x = x32.astype(np.float64)
+    v != argmax of e^{z_v}).  The logits are taken as fp32 (what wedlm_score
+    reads) unless as_f32 is False."""
+    x = np.asarray(logit_row, dtype=np.float32 if as_f32 else np.float64)
+    tok = int(np.argmax(x))                        # first maximum
+    x = x.astype(np.float64)
     z = (x - x[tok]) / temperature
     rest = np.delete(z, tok)
     log_z = math.log1p(float(np.exp(rest).sum()))
@@ -232,6 +237,31 @@ def score(logits: np.ndarray, n_obs: int, temperature: float):
 # --------------------------------------------------------------------------
 # Algorithm 1: commit, SelectByEntropy (Eq. 11), Sample, refill
 # --------------------------------------------------------------------------
+
+def lm_head_score(hidden_bits: np.ndarray, w_bits: np.ndarray,
+                  temperature: float, rows: Optional[Sequence[int]] = None,
+                  chunk: int = 8192):
+    """Output layer plus score: logits[r, v] = sum_k hidden[r, k] * W[v, k]
+    exactly in fp64 from the bf16-decoded inputs (hidden [R, Hd], W [V, Hd],
+    the output layer's weight as stored, one row per token), then the
+    greedy token, entropy and top probability of softmax(logits / T) of
+    each row, on the fp64 logits.  `rows` limits the work to sampled rows;
+    the vocabulary is processed in chunks to bound memory.
+    Returns (tok [n], H [n], p_max [n]) for the rows in order."""
+    h = bf16_to_f64(np.asarray(hidden_bits))
+    rr = list(range(h.shape[0])) if rows is None else list(rows)
+    hs = h[rr]
+    V = w_bits.shape[0]
+    logits = np.empty((len(rr), V))
+    for v0 in range(0, V, chunk):
+        w = bf16_to_f64(np.asarray(w_bits[v0:v0 + chunk]))
+        logits[:, v0:v0 + w.shape[0]] = hs @ w.T
+    out = [score_row(row, temperature, as_f32=False) for row in logits]
+    tok = np.array([o[0] for o in out], dtype=np.int64)
+    H = np.array([o[1] for o in out])
+    pm = np.array([o[2] for o in out])
+    return tok, H, pm
+
 
 def slot_of(block_table_row: Sequence[int], pos: int) -> int:
     """Cache slot of logical position `pos` in 16-token pages."""

@@ -344,6 +344,35 @@ def decision_inputs(B: int, W: int, Hkv: int, D: int, seed: int, step: int,
     return h.astype(np.float32), tok, k, v
 
 
+def lm_head_inputs(R: int, Hd: int, V: int, seed: int = 0,
+                   kind: str = "normal", spike_frac: float = 0.5,
+                   spike: float = 1.5):
+    """Inputs of the fused output layer + score: hidden [R, Hd] and the
+    vocabulary matrix W [V, Hd] (one row per token), bf16 bits.
+
+    kind "normal": hidden ~ N(0, 1) and W ~ N(0, 1/Hd), so logits are about
+    N(0, 1); a share `spike_frac` of the rows gets hidden += spike * W[t] /
+    |W[t]|^2 for a random token t, lifting that logit by about `spike`.
+    kind "exact": small integers times powers of two (hidden in {-1,0,1}/8,
+    W in {-3..3}/32), so every product and every partial sum of a row is a
+    multiple of 2^-8 below 2^6 in magnitude: exact in fp32 in any order."""
+    rng = rng_for(seed, 200, 0, _P_DECISION)
+    if kind == "exact":
+        h = rng.integers(-1, 2, size=(R, Hd)).astype(np.float32) / 8.0
+        w = rng.integers(-3, 4, size=(V, Hd)).astype(np.float32) / 32.0
+        return f32_to_bf16_bits(h), f32_to_bf16_bits(w)
+    w = (rng.standard_normal((V, Hd), dtype=np.float32) /
+         np.float32(np.sqrt(Hd)))
+    wb = f32_to_bf16_bits(w)
+    h = rng.standard_normal((R, Hd), dtype=np.float32)
+    sp = np.nonzero(rng.random(R) < spike_frac)[0]
+    toks = rng.integers(0, V, size=len(sp))
+    for r, t in zip(sp, toks):
+        wt = (wb[t].astype(np.uint32) << 16).view(np.float32)
+        h[r] += np.float32(spike) * wt / np.float32((wt.astype(np.float64) ** 2).sum())
+    return f32_to_bf16_bits(h), wb
+
+
 def gather_prefix(k_cache: np.ndarray, v_cache: np.ndarray, bt: np.ndarray,
                   b: int, c: int):
     """Read sequence b's first c cache positions back into logical order,

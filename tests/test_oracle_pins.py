@@ -14,6 +14,7 @@ import numpy as np
 import pytest
 
 from oracle import wedlm_oracle as O
+from paper_2512_22737_amd import workloads as WL
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -582,3 +583,77 @@ def test_stream_batch_independence():
             toks += rr["committed"]
             win, c = rr["win"], rr["c"]
         assert toks == r["tokens"][b]
+
+
+# --------------------------------------------------------------------------
+# output layer + score (the fused LM-head kernel's definition)
+# --------------------------------------------------------------------------
+
+def _bf16(x):
+    return WL.f32_to_bf16_bits(np.asarray(x, dtype=np.float32))
+
+
+def test_lm_head_zero_hidden_is_uniform():
+    """hidden = 0: every logit is 0, so the distribution is uniform over V:
+    H = ln V, p_max = 1/V, token 0 (the first maximum)."""
+    V, Hd = 37, 16
+    rng = np.random.default_rng(0)
+    tok, H, pm = O.lm_head_score(_bf16(np.zeros((2, Hd))),
+                                 _bf16(rng.standard_normal((V, Hd))), 0.1)
+    assert list(tok) == [0, 0]
+    assert np.allclose(H, math.log(V), rtol=1e-12)
+    assert np.allclose(pm, 1.0 / V, rtol=1e-12)
+
+
+def test_lm_head_one_hot_vocabulary_selects_hidden_entries():
+    """W = identity rows (V <= Hd): logits are the hidden entries 0..V-1, so
+    the result is the score of those numbers."""
+    V, Hd = 12, 16
+    rng = np.random.default_rng(1)
+    h = _bf16(rng.standard_normal((3, Hd)))
+    tok, H, pm = O.lm_head_score(h, _bf16(np.eye(V, Hd)), 0.5)
+    x = O.bf16_to_f64(h)[:, :V]
+    for r in range(3):
+        t2, H2, p2 = O.score_row(x[r], 0.5, as_f32=False)
+        assert tok[r] == int(np.argmax(x[r])) == t2
+        assert H[r] == pytest.approx(H2, rel=1e-13)
+        assert pm[r] == pytest.approx(p2, rel=1e-13)
+
+
+def test_lm_head_exact_inputs_against_integer_dot_products():
+    """The "exact" recipe: hidden*8 and W*32 are small integers, so every
+    logit*256 is an integer; Python integer dot products (no floating point)
+    give the logits, and ties between equal logits go to the lower id."""
+    R, Hd, V = 5, 64, 300
+    hb, wb = WL.lm_head_inputs(R, Hd, V, seed=3, kind="exact")
+    hi = np.rint(O.bf16_to_f64(hb) * 8).astype(np.int64)
+    wi = np.rint(O.bf16_to_f64(wb) * 32).astype(np.int64)
+    tok, H, pm = O.lm_head_score(hb, wb, 0.1, chunk=37)
+    for r in range(R):
+        lg = [sum(int(a) * int(b) for a, b in zip(hi[r], wi[v]))
+              for v in range(V)]
+        best = max(lg)
+        assert tok[r] == lg.index(best)
+        t2, H2, p2 = O.score_row(np.array(lg, dtype=np.float64) / 256.0, 0.1,
+                                 as_f32=False)
+        assert H[r] == pytest.approx(H2, rel=1e-13, abs=1e-300)
+        assert pm[r] == pytest.approx(p2, rel=1e-13)
+
+
+def test_lm_head_rows_and_chunks_do_not_change_results():
+    R, Hd, V = 6, 32, 101
+    hb, wb = WL.lm_head_inputs(R, Hd, V, seed=4)
+    full = O.lm_head_score(hb, wb, 0.1)
+    part = O.lm_head_score(hb, wb, 0.1, rows=[4, 1], chunk=10)
+    assert list(part[0]) == [full[0][4], full[0][1]]
+    assert np.array_equal(part[1], full[1][[4, 1]])
+
+
+def test_lm_head_spiked_rows_pick_their_token():
+    """The "normal" recipe lifts one logit of a spiked row by about the
+    spike; with a large spike that token is the greedy one."""
+    R, Hd, V = 8, 256, 500
+    hb, wb = WL.lm_head_inputs(R, Hd, V, seed=5, spike_frac=1.0, spike=30.0)
+    tok, H, pm = O.lm_head_score(hb, wb, 0.1)
+    # the spiked token wins by a wide margin: p_max near 1
+    assert (pm > 0.99).all()
