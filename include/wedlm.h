@@ -258,6 +258,37 @@ int wedlm_commit_rule(int32_t* win_tok, int32_t* win_start,
                       void* stream);
 
 /* Message for a WEDLM_* return code (static storage). */
+/*
+ * wedlm_lm_head_score -- the output layer of the window forward fused with
+ * the score of its rows: the logits that the mask slots are scored on
+ * (Algorithm 1's Forward and SelectByEntropy; the H_i of Eq. (11),
+ * Sec. 5.2), reduced to the greedy token, entropy and top probability
+ * without writing the logits to memory.
+ *
+ * For each row r:  logits[v] = sum_k hidden[r][k] * w_vocab[v][k] (bf16
+ * products, fp32 accumulation on MFMA), then with p = softmax(logits / T):
+ *   argmax[r]  = the first v holding the largest logit (fp32)
+ *   entropy[r] = -sum_v p_v ln p_v (nats), pmax[r] = max_v p_v
+ *
+ * In:
+ *   hidden   [R, Hd] bf16   rows to score (e.g. the final hidden states of
+ *                           the window's mask rows), row-major
+ *   w_vocab  [V, Hd] bf16   output-layer weight, one row per token
+ *   Hd a multiple of 64; R, V >= 1; temperature > 0
+ * Out:
+ *   argmax [R] int32, entropy [R] fp32, pmax [R] fp32 or NULL
+ * Workspace: wedlm_lm_head_score_workspace_size(R, Hd, V) bytes (0 when the
+ *   vocabulary fits one tile); per-tile partial states, contents undefined.
+ * Errors: WEDLM_E_ARG (NULL pointer, temperature), WEDLM_E_SHAPE,
+ *   WEDLM_E_WORKSPACE, WEDLM_E_LAUNCH.
+ */
+size_t wedlm_lm_head_score_workspace_size(int32_t R, int32_t Hd, int32_t V);
+int wedlm_lm_head_score(const uint16_t* hidden, const uint16_t* w_vocab,
+                        int32_t R, int32_t Hd, int32_t V, double temperature,
+                        int32_t* argmax, float* entropy, float* pmax,
+                        void* workspace, size_t workspace_bytes,
+                        void* stream);
+
 const char* wedlm_strerror(int code);
 
 /* Library version, major * 10000 + minor * 100 + patch. */

@@ -64,6 +64,11 @@ def _load():
                                       I32, I32, I32, I32, I32, P, P, P, P, P,
                                       I32, P]
     lib.wedlm_commit_rule.restype = ctypes.c_int
+    lib.wedlm_lm_head_score_workspace_size.argtypes = [I32, I32, I32]
+    lib.wedlm_lm_head_score_workspace_size.restype = SZ
+    lib.wedlm_lm_head_score.argtypes = [P, P, I32, I32, I32, D_, P, P, P, P,
+                                        SZ, P]
+    lib.wedlm_lm_head_score.restype = ctypes.c_int
     lib.wedlm_strerror.argtypes = [ctypes.c_int]
     lib.wedlm_strerror.restype = ctypes.c_char_p
     lib.wedlm_version.argtypes = []
@@ -78,8 +83,9 @@ def lib():
 
 EXPORTED = ["wedlm_reorder", "wedlm_window_attn_workspace_size",
             "wedlm_window_attn", "wedlm_score_workspace_size", "wedlm_score",
-            "wedlm_commit", "wedlm_commit_rule", "wedlm_strerror",
-            "wedlm_version"]
+            "wedlm_commit", "wedlm_commit_rule",
+            "wedlm_lm_head_score_workspace_size", "wedlm_lm_head_score",
+            "wedlm_strerror", "wedlm_version"]
 
 # decoding rules of wedlm_commit_rule (include/wedlm.h)
 RULE_STREAMING, RULE_BLOCK, RULE_ONE_TOKEN = 0, 1, 2
@@ -209,6 +215,33 @@ def wedlm_score(logits, n_obs, temperature: float, argmax, entropy,
         _t(pmax, "pmax", f32, (B, W), allow_none=True), ws_ptr, ws_bytes,
         _stream())
     _check(code, "wedlm_score")
+
+
+def wedlm_lm_head_score_workspace_size(R, Hd, V) -> int:
+    return int(_load().wedlm_lm_head_score_workspace_size(R, Hd, V))
+
+
+def wedlm_lm_head_score(hidden, w_vocab, temperature: float, argmax, entropy,
+                        pmax=None, workspace=None) -> None:
+    """hidden [R, Hd] bf16, w_vocab [V, Hd] bf16 -> argmax [R] int32,
+    entropy [R] fp32, pmax [R] fp32 (optional).  A workspace of at least
+    wedlm_lm_head_score_workspace_size(R, Hd, V) bytes is allocated here if
+    none is given."""
+    R, Hd = hidden.shape
+    V = w_vocab.shape[0]
+    need = wedlm_lm_head_score_workspace_size(R, Hd, V)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=hidden.device)
+    ws_ptr = None if workspace is None else workspace.data_ptr()
+    ws_bytes = 0 if workspace is None else workspace.numel()
+    code = _load().wedlm_lm_head_score(
+        _t(hidden, "hidden", _BF16, (R, Hd)),
+        _t(w_vocab, "w_vocab", _BF16, (V, Hd)), R, Hd, V, float(temperature),
+        _t(argmax, "argmax", (torch.int32,), (R,)),
+        _t(entropy, "entropy", (torch.float32,), (R,)),
+        _t(pmax, "pmax", (torch.float32,), (R,), allow_none=True),
+        ws_ptr, ws_bytes, _stream())
+    _check(code, "wedlm_lm_head_score")
 
 
 def _commit_args(win_tok, win_start, argmax, entropy, tau, lam, k_phys,
