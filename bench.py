@@ -14,6 +14,12 @@ the dominant kernel (window attention: algorithmic bytes per launch over its
 HIP-event-timed average duration, against 8 TB/s), and the fp64 CPU oracle
 timed on a bounded sample of the same workload.
 
+--lm-head instead times wedlm_lm_head_score (the output layer fused with
+the row score) at the Qwen3-8B output-layer shape (Hd 4096, V 151936) for
+several row counts and prints one JSON line per count with its roofline
+(intensity R flop per weight byte: HBM-bound below the ridge, MFMA-bound
+above it).
+
 --compare-rules instead runs the streaming workload (16 sequences, starting
 prefix 1024, W=32, V=151936, fresh synthetic logits every step) under each
 decoding rule of wedlm_commit_rule (Algorithm 1's streaming commit,
@@ -113,6 +119,70 @@ def cpu_baseline(wl, d, seed):
                        f"{len(os.sched_getaffinity(0))} cores")}
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def bench_lm_head(args, dev):
+    """wedlm_lm_head_score at Hd 4096, V 151936 (synthetic "normal" inputs),
+    rows R in 16 (a C2-like step's masked rows), 128, 384 (long_prefix's
+    masked rows) and 1024.  Warmup, then the average of 20 back-to-back
+    launches timed with HIP events on the launch stream."""
+    import numpy as np
+    import torch
+    from paper_2512_22737_amd import wedlm
+    from paper_2512_22737_amd import workloads as WL
+    Hd, V, T = 4096, 151936, 0.1
+    rmax = 1024
+    print("# generating the vocabulary matrix", file=sys.stderr, flush=True)
+    hb, wb = WL.lm_head_inputs(rmax, Hd, V, seed=args.seed)
+
+    def up(a):
+        return (torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+                .view(torch.int16).view(torch.bfloat16))
+
+    h_all, w = up(hb), up(wb)
+    for R in (16, 128, 384, 1024):
+        h = h_all[:R].contiguous()
+        am = torch.empty(R, dtype=torch.int32, device=dev)
+        H = torch.empty(R, dtype=torch.float32, device=dev)
+        pm = torch.empty(R, dtype=torch.float32, device=dev)
+        ws = torch.empty(max(wedlm.wedlm_lm_head_score_workspace_size(R, Hd, V),
+                             1), dtype=torch.uint8, device=dev)
+        run = lambda: wedlm.wedlm_lm_head_score(h, w, T, am, H, pm, ws)
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+        n = 20
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / n * 1e3
+        flops = 2.0 * R * Hd * V
+        groups = -(-R // 128)
+        w_bytes = V * Hd * 2
+        alg_bytes = w_bytes + R * Hd * 2 + R * 12
+        tflops = flops / us / 1e6
+        gbps = alg_bytes / us / 1e3
+        # intensity R flop per weight byte against the ridge (312 flop/B)
+        mfma_bound = R > MFMA_BF16_PEAK_TFLOPS * 1e3 / HBM_PEAK_GBPS
+        roof = ({"bound": "mfma", "achieved": tflops,
+                 "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                 "frac": tflops / MFMA_BF16_PEAK_TFLOPS}
+                if mfma_bound else
+                {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS,
+                 "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS})
+        print(json.dumps({
+            "kind": "lm_head_score", "R": R, "Hd": Hd, "V": V,
+            "temperature": T, "us": us, "tflops": tflops,
+            "weight_gbps": w_bytes / us / 1e3, "row_groups": groups,
+            "alg_bytes": alg_bytes, "flops": flops, "roofline": roof}),
+            flush=True)
+
+
 def compare_rules(args, dev):
     """Decoding rules on the streaming workload: every run starts from the
     same all-mask windows at prefix 1024 and draws the same per-step logits
@@ -201,6 +271,8 @@ def main():
                     help="p_cache and committed tokens/s of the decoding "
                          "rules on the streaming workload, then exit")
     ap.add_argument("--rule-steps", type=int, default=128)
+    ap.add_argument("--lm-head", action="store_true",
+                    help="time the fused output layer + score, then exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for "
                          "scaling HBM counters) and exit")
@@ -232,6 +304,9 @@ def main():
 
     if args.compare_rules:
         compare_rules(args, dev)
+        return
+    if args.lm_head:
+        bench_lm_head(args, dev)
         return
 
     wl = WL.WORKLOADS[args.workload]

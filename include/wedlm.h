@@ -274,7 +274,7 @@ int wedlm_commit_rule(int32_t* win_tok, int32_t* win_start,
  *   hidden   [R, Hd] bf16   rows to score (e.g. the final hidden states of
  *                           the window's mask rows), row-major
  *   w_vocab  [V, Hd] bf16   output-layer weight, one row per token
- *   Hd a multiple of 64; R, V >= 1; temperature > 0
+ *   Hd a multiple of 256; R, V >= 1; temperature > 0
  * Out:
  *   argmax [R] int32, entropy [R] fp32, pmax [R] fp32 or NULL
  * Workspace: wedlm_lm_head_score_workspace_size(R, Hd, V) bytes (0 when the

@@ -4,9 +4,13 @@
 // produces the logits the mask slots are scored on).  The fp32 logits are
 // never written to memory.
 //
-// Work decomposition:
-//   workgroup = (256-row vocabulary tile, group of 32*NB hidden rows); eight
-//               waves, wave w owns vocabulary rows 32w .. 32w+31 of the tile
+// Work decomposition (persistent, balanced):
+//   grid      = n_rg row groups x n_slot slots, sized from the occupancy so
+//               that every workgroup is resident at once
+//   wave      = stream j = slot*8 + wave of its row group; it owns the
+//               contiguous vocabulary range [j*V/S, (j+1)*V/S) (S = 8 n_slot
+//               streams), so ranges differ by at most one row, and walks it
+//               in 32-row blocks, keeping a running score state per row
 //   MFMA      = v_mfma_f32_32x32x16_bf16 computing logits^T: A = 32 weight
 //               rows x 16 k (registers), B = 16 k x 32 hidden rows (LDS)
 //   k order   = the contraction runs over k in a permuted order that is the
@@ -15,14 +19,16 @@
 //               for a whole step is then 64 contiguous bytes of its weight
 //               row (four 16-byte loads), the B operand 16 contiguous bytes
 //               of an LDS row.
-// Memory path: the weights are the HBM stream (V * Hd * 2 bytes per launch,
-//   read once per row group); each wave streams its own rows straight into
-//   registers, PF steps ahead.  The hidden rows of a step go through LDS
-//   (XOR-swizzled 16-byte chunks), double-buffered, one barrier per step.
-// Epilogue: a lane holds 16 logits of one hidden row per row block; they
-//   enter the online score state of score_state.h, states merge across the
-//   two lane halves, the eight waves (LDS) and the vocabulary tiles (a merge
-//   kernel over a workspace of per-tile states).
+// Memory path: the weights are the HBM stream (V * Hd * 2 bytes per row
+//   group); each wave streams its own rows straight into registers, PF steps
+//   ahead, across block boundaries.  The hidden rows of a step go through
+//   LDS (XOR-swizzled 16-byte chunks), double-buffered, one barrier per step.
+//   Slots are placed so that the row groups of one slot share an XCD (and
+//   the weights they stream in its L2).
+// Epilogue: after each block a lane holds 16 logits of one hidden row per
+//   row block; they enter the wave's running state (score_state.h), merged
+//   across the two lane halves; at the end the eight waves merge in LDS and
+//   the slots in a merge kernel over a workspace of per-slot states.
 // Roofline: 2 * R * Hd * V flops against V * Hd * 2 weight bytes per row
 //   group; R rows in one group give an intensity of R flop/byte.
 #include "common.h"
@@ -34,7 +40,6 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * kWave;
-constexpr int kVocabTile = 32 * kWaves;   // vocabulary rows per workgroup
 constexpr int kKStep = 64;                // k per pipeline step
 constexpr int kPF = 4;                    // weight steps in flight per wave
 
@@ -42,12 +47,13 @@ struct LmArgs {
   const uint16_t* hidden;   // [R, Hd]
   const uint16_t* w;        // [V, Hd]
   int R, Hd, V;
-  int n_vt, n_rg;           // vocabulary tiles, row groups
+  int n_rg, n_slot;         // row groups, slots (per row group)
+  int nblk;                 // 32-row vocabulary blocks per stream
   double c2;                // log2(e) / T
   int32_t* argmax;
   float* entropy;
   float* pmax;
-  State* ws;                // [R, n_vt] (n_vt > 1)
+  State* ws;                // [R, n_slot] (n_slot > 1)
 };
 
 // LDS row of one k step: 64 bf16 = eight 16-byte chunks; chunk c of row r
@@ -65,156 +71,185 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   constexpr int kLds = 2 * kStage > kRed ? 2 * kStage : kRed;
   __shared__ __attribute__((aligned(16))) char smem[kLds];
 
-  // tiles in vocabulary-major order, row groups inner; workgroups of one
-  // XCD (blockIdx % 8) take a contiguous range, so the row groups of a
-  // vocabulary tile run on the same XCD and share its weights in L2
-  const int n_tiles = a.n_vt * a.n_rg;
-  const int per_xcd = (n_tiles + 7) / 8;
-  const int tile = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (tile >= n_tiles) return;
-  const int vt = tile / a.n_rg;
-  const int rg = tile % a.n_rg;
+  const int xcd = blockIdx.x % 8;
+  const int local = blockIdx.x / 8;
+  const int rg = local % a.n_rg;
+  const int slot = (local / a.n_rg) * 8 + xcd;
+  if (slot >= a.n_slot) return;
 
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
   const int col = lane & 31;
   const int hf = lane >> 5;
-  const int v_wave = vt * kVocabTile + wave * 32;   // first vocab row of wave
   const int row0 = rg * RG;                         // first hidden row
+  const int64_t S = static_cast<int64_t>(a.n_slot) * kWaves;
+  const int64_t j = static_cast<int64_t>(slot) * kWaves + wave;
+  const int v_lo = static_cast<int>(j * a.V / S);
+  const int v_hi = static_cast<int>((j + 1) * a.V / S);
+  const int nsteps = a.Hd / kKStep;                 // a multiple of kPF
+  const int nblk = a.nblk;
+  const int total = nblk * nsteps;
 
-  // ---- weights: lane streams row v_wave + col, bytes 64*hf .. 64*hf+63 of
-  // each 128-byte k step (rows past V re-read row V-1; masked later)
-  const int vrow = min(v_wave + col, a.V - 1);
-  const uint16_t* wp = a.w + static_cast<int64_t>(vrow) * a.Hd + hf * 32;
-  const int nsteps = a.Hd / kKStep;
+  // ---- weights: in block bi the lane streams row v_lo + 32 bi + col, bytes
+  // 64*hf .. 64*hf+63 of each 128-byte k step.  Every load is issued (no
+  // branch in the step, so the compiler's waits stay partial): a row past
+  // the stream's range re-reads its last row (a line another lane loads
+  // anyway) and its logits are masked; steps past the end re-read the last.
+  const uint16_t* wbase = a.w + hf * 32;
+  const int v_last = max(v_hi - 1, 0);
   u16x8_t wa[kPF][4];
-  auto wload = [&](int s, u16x8_t (&r)[4]) {
-    const uint16_t* p = wp + s * kKStep;
+  auto wload = [&](int q, u16x8_t (&r)[4]) {
+    q = min(q, total - 1);
+    const int bi = q / nsteps;
+    const int s = q - bi * nsteps;
+    const int v = min(v_lo + 32 * bi + col, v_last);
+    const uint16_t* p = wbase + static_cast<int64_t>(v) * a.Hd + s * kKStep;
+    // plain loads: the four loads of a step share each 128-byte line, and
+    // a non-temporal hint would fetch the line once per load
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      r[j] = __builtin_nontemporal_load(
-          reinterpret_cast<const u16x8_t*>(p + j * 8));
+    for (int u = 0; u < 4; ++u)
+      r[u] = *reinterpret_cast<const u16x8_t*>(p + u * 8);
   };
 
   // ---- hidden rows: thread t moves 16-byte chunks t, t+512, ... of the
-  // step's RG x 128 bytes (rows past R re-read row R-1; never written out)
+  // step's RG x 128 bytes, modulo RG*8 (when RG*8 < 512 two threads write the
+  // same chunk with the same bytes); rows past R re-read row R-1 and are
+  // never written out
   constexpr int kChunks = RG * 8;
   constexpr int kCPT = (kChunks + kThreads - 1) / kThreads;
   int h_src[kCPT], h_dst[kCPT];
-  bool h_on[kCPT];
 #pragma unroll
   for (int u = 0; u < kCPT; ++u) {
-    const int g = threadIdx.x + u * kThreads;
-    h_on[u] = g < kChunks;
-    const int r = h_on[u] ? g / 8 : 0;
+    const int g = (threadIdx.x + u * kThreads) % kChunks;
+    const int r = g / 8;
     const int c = g % 8;
     const int hr = min(row0 + r, a.R - 1);
     h_src[u] = hr * a.Hd + c * 8;        // element offset within step 0
     h_dst[u] = h_off(r, c);
   }
-  u16x8_t hreg[kCPT];
-  auto hload = [&](int s) {
+  // a ring of kPF register stages: step s's rows live in stage s % kPF,
+  // loaded kPF steps before they go to LDS (L2 latency hidden)
+  u16x8_t hreg[kPF][kCPT];
+  auto hload = [&](int s, u16x8_t (&r)[kCPT]) {
 #pragma unroll
     for (int u = 0; u < kCPT; ++u)
-      if (h_on[u])
-        hreg[u] = *reinterpret_cast<const u16x8_t*>(a.hidden + h_src[u] +
-                                                    s * kKStep);
+      r[u] = *reinterpret_cast<const u16x8_t*>(a.hidden + h_src[u] +
+                                               s * kKStep);
   };
-  auto hstore = [&](char* sb) {
+  auto hstore = [&](char* sb, const u16x8_t (&r)[kCPT]) {
 #pragma unroll
     for (int u = 0; u < kCPT; ++u)
-      if (h_on[u]) *reinterpret_cast<u16x8_t*>(sb + h_dst[u]) = hreg[u];
+      *reinterpret_cast<u16x8_t*>(sb + h_dst[u]) = r[u];
   };
+  auto hstep = [&](int s) { return s % nsteps; };
 
   floatx16_t acc[NB];
+  auto zero_acc = [&]() {
 #pragma unroll
-  for (int b = 0; b < NB; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[b][e] = 0.f;
+      for (int e = 0; e < 16; ++e) acc[b][e] = 0.f;
+  };
+  zero_acc();
+  State st[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) st[b] = empty_state();
 
-  // prologue: weights of steps 0..PF-1 in flight, hidden step 0 in LDS,
-  // hidden step 1 in registers
+  // prologue: hidden step 0 into LDS, then the loads of four steps issued
+  // in the steady-state order (weights of step p, then hidden step p+1 into
+  // stage (p+1) % PF), so the loop head sees the same loads in flight from
+  // both of its predecessors and the compiler's waits stay partial
+  hload(0, hreg[0]);
+  hstore(smem, hreg[0]);
 #pragma unroll
-  for (int p = 0; p < kPF; ++p) wload(min(p, nsteps - 1), wa[p]);
-  hload(0);
-  hstore(smem);
-  if (nsteps > 1) hload(1);
+  for (int p = 0; p < kPF; ++p) {
+    wload(p, wa[p]);
+    hload(hstep(p + 1), hreg[(p + 1) % kPF]);
+  }
   __syncthreads();
 
-  // step s: B fragments from LDS buffer s&1, A from register stage s%PF;
-  // then the next hidden step goes to the other buffer and the stage is
-  // refilled with step s+PF.  One barrier per step: the buffer written in
-  // step s was last read in step s-1, before that step's barrier.
-  auto step = [&](const int j, const int s) __attribute__((always_inline)) {
-    const char* sb = smem + (j & 1) * kStage;
+  // step q = bi*nsteps + s (u = s % kPF, static): B fragments from LDS
+  // buffer s&1 (nsteps is even), A from register stage u; then the stage is
+  // refilled with step q+PF, hidden step s+1 (register stage u+1) goes to
+  // the other LDS buffer and that stage is refilled with step s+1+PF
+  // (unconditionally: past the last step these are re-reads nobody uses).
+  // One barrier per step: the buffer written in step q was last read in
+  // step q-1, before its barrier.
+  auto step = [&](const int u, const int q, const int s)
+      __attribute__((always_inline)) {
+    const char* sb = smem + (u & 1) * kStage;
+    bf16x8_t bfr[4][NB];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const bf16x8_t af = __builtin_bit_cast(bf16x8_t, wa[j % kPF][kk]);
+    for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const bf16x8_t bfr = __builtin_bit_cast(
+      for (int b = 0; b < NB; ++b)
+        bfr[kk][b] = __builtin_bit_cast(
             bf16x8_t, *reinterpret_cast<const u16x8_t*>(
                           sb + h_off(b * 32 + col, hf * 4 + kk)));
-        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bfr, acc[b], 0,
-                                                         0, 0);
-      }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const bf16x8_t af = __builtin_bit_cast(bf16x8_t, wa[u][kk]);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bfr[kk][b],
+                                                         acc[b], 0, 0, 0);
     }
-    wload(min(s + kPF, nsteps - 1), wa[j % kPF]);
-    if (s + 1 < nsteps) {
-      hstore(smem + ((j + 1) & 1) * kStage);
-      if (s + 2 < nsteps) hload(s + 2);
-    }
+    wload(q + kPF, wa[u]);
+    hstore(smem + ((u + 1) & 1) * kStage, hreg[(u + 1) % kPF]);
+    hload(hstep(s + 1 + kPF), hreg[(u + 1) % kPF]);
     __syncthreads();
   };
-  constexpr int U = kPF % 2 == 0 ? kPF : 2 * kPF;
-  const int nfull = nsteps / U * U;
-  for (int s0 = 0; s0 < nfull; s0 += U) {
+
+  for (int bi = 0; bi < nblk; ++bi) {
+    for (int s0 = 0; s0 < nsteps; s0 += kPF) {
 #pragma unroll
-    for (int j = 0; j < U; ++j) step(j, s0 + j);
-  }
+      for (int u = 0; u < kPF; ++u)
+        step(u, bi * nsteps + s0 + u, s0 + u);
+    }
+    // block done: lane (col, hf) of row block b holds logits of hidden row
+    // row0 + 32b + col at vocabulary rows v0 + 8*(e/4) + 4*hf + e%4
+    const int v0 = v_lo + 32 * bi;
 #pragma unroll
-  for (int j = 0; j < U - 1; ++j) {
-    if (nfull + j >= nsteps) break;
-    step(j, nfull + j);
+    for (int b = 0; b < NB; ++b) {
+      float x[16];
+      int idx[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int v = v0 + 8 * (e >> 2) + 4 * hf + (e & 3);
+        idx[e] = v;
+        x[e] = v < v_hi ? acc[b][e] : kNegInf;
+      }
+      push_block(st[b], x, idx, a.c2);
+    }
+    zero_acc();
   }
 
-  // ---- epilogue: lane (col, hf) of row block b holds logits of hidden row
-  // row0 + 32b + col at vocabulary rows v_wave + 8*(e/4) + 4*hf + e%4
+  // ---- the waves' states: both lane halves, then the eight waves in LDS
   State* red = reinterpret_cast<State*>(smem);       // [kWaves][RG]
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    float x[16];
-    int idx[16];
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int v = v_wave + 8 * (e >> 2) + 4 * hf + (e & 3);
-      idx[e] = v;
-      x[e] = v < a.V ? acc[b][e] : kNegInf;
-    }
-    State st = empty_state();
-    push_block(st, x, idx, a.c2);
-    merge(st, shfl_xor_state(st, 32), a.c2);
-    if (hf == 0) red[wave * RG + b * 32 + col] = st;
+    merge(st[b], shfl_xor_state(st[b], 32), a.c2);
+    if (hf == 0) red[wave * RG + b * 32 + col] = st[b];
   }
   __syncthreads();
   if (threadIdx.x < RG) {
     const int r = threadIdx.x;
-    State st = red[r];
-    for (int w = 1; w < kWaves; ++w) merge(st, red[w * RG + r], a.c2);
+    State m = red[r];
+    for (int w = 1; w < kWaves; ++w) merge(m, red[w * RG + r], a.c2);
     const int row = row0 + r;
     if (row < a.R) {
-      if (a.n_vt == 1) finish(st, row, a.argmax, a.entropy, a.pmax);
-      else a.ws[static_cast<int64_t>(row) * a.n_vt + vt] = st;
+      if (a.n_slot == 1) finish(m, row, a.argmax, a.entropy, a.pmax);
+      else a.ws[static_cast<int64_t>(row) * a.n_slot + slot] = m;
     }
   }
 }
 
-// Merge the vocabulary-tile states of each row, lanes over tiles.
+// Merge the slot states of each row, lanes over slots.
 __global__ __launch_bounds__(kWave) void lm_head_merge_kernel(LmArgs a) {
   const int row = blockIdx.x;
   State st = empty_state();
-  const State* p = a.ws + static_cast<int64_t>(row) * a.n_vt;
-  for (int t = lane_id(); t < a.n_vt; t += kWave) merge(st, p[t], a.c2);
+  const State* p = a.ws + static_cast<int64_t>(row) * a.n_slot;
+  for (int t = lane_id(); t < a.n_slot; t += kWave) merge(st, p[t], a.c2);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1)
     merge(st, shfl_xor_state(st, off), a.c2);
@@ -228,19 +263,66 @@ int blocks_per_wave(int R) {
   return nb < 4 ? nb : 4;
 }
 
+// Hd a multiple of 4 k steps: the weight stages then line up with the steps
+// of every block.
 bool lm_shape_ok(int R, int Hd, int V) {
-  return R >= 1 && Hd >= kKStep && Hd % kKStep == 0 && V >= 1 &&
+  return R >= 1 && Hd >= kKStep * kPF && Hd % (kKStep * kPF) == 0 && V >= 1 &&
          static_cast<int64_t>(V) * Hd < (1ll << 40) &&
          static_cast<int64_t>(R) * Hd < (1ll << 31);
+}
+
+template <int NB>
+int resident_per_cu() {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &n, reinterpret_cast<const void*>(lm_head_kernel<NB>),
+          kThreads, 0) != hipSuccess || n < 1)
+    n = 1;
+  return n;
+}
+
+// Slots per row group: every workgroup resident at once (CUs x occupancy),
+// no more streams than 32-row blocks.  Cached per device.
+struct LmPlan {
+  int nb, n_rg, n_slot, nblk;
+};
+
+bool lm_plan(int R, int Hd, int V, LmPlan* p) {
+  if (!lm_shape_ok(R, Hd, V)) return false;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+  static int cus[64], occ[64][5];
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount,
+                              dev) != hipSuccess || n < 1)
+      return false;
+    occ[dev][1] = resident_per_cu<1>();
+    occ[dev][2] = resident_per_cu<2>();
+    occ[dev][3] = resident_per_cu<3>();
+    occ[dev][4] = resident_per_cu<4>();
+    cus[dev] = n;
+  }
+  p->nb = blocks_per_wave(R);
+  p->n_rg = (R + 32 * p->nb - 1) / (32 * p->nb);
+  int n_slot = cus[dev] * occ[dev][p->nb] / p->n_rg;
+  const int by_blocks = (V + 32 * kWaves - 1) / (32 * kWaves);
+  if (n_slot > by_blocks) n_slot = by_blocks;
+  if (n_slot < 1) n_slot = 1;
+  p->n_slot = n_slot;
+  const int64_t S = static_cast<int64_t>(n_slot) * kWaves;
+  const int64_t per = (V + S - 1) / S;               // rows of the longest
+  p->nblk = static_cast<int>((per + 31) / 32);
+  return true;
 }
 
 }  // namespace
 
 extern "C" size_t wedlm_lm_head_score_workspace_size(int32_t R, int32_t Hd,
                                                      int32_t V) {
-  if (!lm_shape_ok(R, Hd, V)) return 0;
-  const int n_vt = (V + kVocabTile - 1) / kVocabTile;
-  return n_vt > 1 ? static_cast<size_t>(R) * n_vt * sizeof(State) : 0;
+  LmPlan p;
+  if (!lm_plan(R, Hd, V, &p)) return 0;
+  return p.n_slot > 1 ? static_cast<size_t>(R) * p.n_slot * sizeof(State) : 0;
 }
 
 extern "C" int wedlm_lm_head_score(const uint16_t* hidden,
@@ -251,29 +333,31 @@ extern "C" int wedlm_lm_head_score(const uint16_t* hidden,
                                    size_t workspace_bytes, void* stream) {
   if (!hidden || !w_vocab || !argmax || !entropy) return WEDLM_E_ARG;
   if (!(temperature > 0.0) || !(temperature < 1e30)) return WEDLM_E_ARG;
+  LmPlan p;
   if (!lm_shape_ok(R, Hd, V)) return WEDLM_E_SHAPE;
-  const size_t need = wedlm_lm_head_score_workspace_size(R, Hd, V);
+  if (!lm_plan(R, Hd, V, &p)) return WEDLM_E_DEVICE;
+  const size_t need =
+      p.n_slot > 1 ? static_cast<size_t>(R) * p.n_slot * sizeof(State) : 0;
   if (workspace_bytes < need || (need && !workspace)) return WEDLM_E_WORKSPACE;
   LmArgs a{};
   a.hidden = hidden; a.w = w_vocab; a.R = R; a.Hd = Hd; a.V = V;
-  a.n_vt = (V + kVocabTile - 1) / kVocabTile;
-  const int nb = blocks_per_wave(R);
-  a.n_rg = (R + 32 * nb - 1) / (32 * nb);
+  a.n_rg = p.n_rg; a.n_slot = p.n_slot; a.nblk = p.nblk;
   a.c2 = 1.4426950408889634074 / temperature;
   a.argmax = argmax; a.entropy = entropy; a.pmax = pmax;
   a.ws = static_cast<State*>(workspace);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int64_t tiles = static_cast<int64_t>(a.n_vt) * a.n_rg;
-  if (tiles > (1ll << 30)) return WEDLM_E_SHAPE;
-  const unsigned grid = static_cast<unsigned>((tiles + 7) / 8 * 8);
-  switch (nb) {
+  // slot = (blockIdx / 8 / n_rg) * 8 + blockIdx % 8: a multiple of 8 per
+  // row group covers every slot
+  const int64_t grid = 8ll * p.n_rg * ((p.n_slot + 7) / 8);
+  if (grid > (1ll << 30)) return WEDLM_E_SHAPE;
+  switch (p.nb) {
     case 1: hipLaunchKernelGGL(lm_head_kernel<1>, dim3(grid), dim3(kThreads), 0, st, a); break;
     case 2: hipLaunchKernelGGL(lm_head_kernel<2>, dim3(grid), dim3(kThreads), 0, st, a); break;
     case 3: hipLaunchKernelGGL(lm_head_kernel<3>, dim3(grid), dim3(kThreads), 0, st, a); break;
     default: hipLaunchKernelGGL(lm_head_kernel<4>, dim3(grid), dim3(kThreads), 0, st, a); break;
   }
   WEDLM_LAUNCH_CHECK();
-  if (a.n_vt > 1) {
+  if (p.n_slot > 1) {
     hipLaunchKernelGGL(lm_head_merge_kernel, dim3(R), dim3(kWave), 0, st, a);
     WEDLM_LAUNCH_CHECK();
   }

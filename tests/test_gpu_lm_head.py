@@ -5,8 +5,9 @@ each row) against the fp64 oracle.
   partial sum is exact in fp32 in any order, so the kernel's logits equal
   the oracle's exactly.  Greedy token bit-exact (ties included), entropy and
   top probability within the score's tolerance.  Shapes cover one and
-  several vocabulary tiles, ragged vocabulary and row tails, one to four
-  32-row blocks per wave, several row groups, and one k step.
+  several 32-row blocks per vocabulary stream, streams shorter than a
+  block, ragged row tails, one to four 32-row blocks of hidden rows per
+  wave, and several row groups.
 * "normal" inputs (N(0,1) hidden, N(0,1/Hd) weights, spiked rows) at the
   Qwen3-8B output-layer shape (Hd 4096, V 151936) on sampled rows: fp32
   accumulation over 4096 products.  Per row the logit error is bounded by
@@ -52,13 +53,14 @@ def _run(hb, wb, T):
 
 EXACT = [
     # R, Hd, V
-    (1, 64, 7),          # one k step, one partial vocabulary tile
-    (5, 128, 256),       # exactly one tile
-    (32, 256, 1000),     # ragged vocabulary tail, one row block
-    (40, 192, 513),      # two row blocks, ragged rows
+    (1, 256, 7),         # one pipeline group of k steps, fewer tokens than lanes
+    (5, 256, 256),       # one 32-row block per stream at most
+    (32, 256, 1000),     # one row block, ragged vocabulary ranges
+    (40, 512, 513),      # two row blocks, ragged rows
     (96, 256, 2047),     # three row blocks
     (128, 512, 3001),    # four row blocks
-    (200, 320, 1500),    # two row groups (128 + 72)
+    (200, 768, 1500),    # two row groups (128 + 72)
+    (17, 1024, 40000),   # several 32-row blocks per stream
 ]
 
 
@@ -113,9 +115,10 @@ def test_lm_head_argument_checks():
     bf = dict(dtype=torch.bfloat16, device="cuda")
     am = torch.empty(2, dtype=torch.int32, device="cuda")
     H = torch.empty(2, dtype=torch.float32, device="cuda")
-    with pytest.raises(wedlm.WedlmError):       # Hd not a multiple of 64
-        wedlm.wedlm_lm_head_score(torch.zeros(2, 96, **bf),
-                                  torch.zeros(10, 96, **bf), 0.1, am, H)
+    for Hd in (96, 320):                       # Hd not a multiple of 256
+        with pytest.raises(wedlm.WedlmError):
+            wedlm.wedlm_lm_head_score(torch.zeros(2, Hd, **bf),
+                                      torch.zeros(10, Hd, **bf), 0.1, am, H)
     with pytest.raises(wedlm.WedlmError):       # temperature
-        wedlm.wedlm_lm_head_score(torch.zeros(2, 64, **bf),
-                                  torch.zeros(10, 64, **bf), 0.0, am, H)
+        wedlm.wedlm_lm_head_score(torch.zeros(2, 256, **bf),
+                                  torch.zeros(10, 256, **bf), 0.0, am, H)
