@@ -154,6 +154,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   State st[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) st[b] = empty_state();
+  const ExpScale sc = exp_scale(a.c2);
 
   // prologue: hidden step 0 into LDS, then the loads of four steps issued
   // in the steady-state order (weights of step p, then hidden step p+1 into
@@ -219,7 +220,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
         idx[e] = v;
         x[e] = v < v_hi ? acc[b][e] : kNegInf;
       }
-      push_block(st[b], x, idx, a.c2);
+      push_block(st[b], x, idx, sc);
     }
     zero_acc();
   }

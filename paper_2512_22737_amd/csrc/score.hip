@@ -69,6 +69,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(ScoreArgs a) {
   const int v0 = ch * a.chunk;
   const int v1 = min(a.V, v0 + a.chunk);
   State st = empty_state();
+  const ExpScale sc = exp_scale(a.c2);
   constexpr int kStep = kThreads * kBlk;       // logits per workgroup step
   int v = v0;
   if (kVec) {
@@ -94,7 +95,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(ScoreArgs a) {
           xs[g * 4 + k] = q[g][k];
           idx[g * 4 + k] = vs + (g * kThreads + threadIdx.x) * 4 + k;
         }
-      push_block(st, xs, idx, a.c2);
+      push_block(st, xs, idx, sc);
     };
     if (nsteps > 0) {
       floatx4_t qa[kBlk / 4], qb[kBlk / 4];
@@ -115,7 +116,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(ScoreArgs a) {
   for (int u = v + threadIdx.x; u < v1; u += kThreads) {
     const float xs[1] = {x[u]};
     const int idx[1] = {u};
-    push_block(st, xs, idx, a.c2);
+    push_block(st, xs, idx, sc);
   }
   st = block_reduce(st, a.c2);
   if (threadIdx.x != 0) return;

@@ -47,16 +47,50 @@ __device__ __forceinline__ float exp2_split(double y) {
   return y > -200.0 ? __builtin_fmaf(e, yl, e) : 0.f;
 }
 
-// One term of the sums: 2^y with y = x*c2 - mc formed in fp64 and clamped
-// at -256 (a -inf logit gives 0, never inf * 0), then split into an fp32
-// head yh (returned, for the S sum) and tail for exp2_split's correction.
-__device__ __forceinline__ float exp2_term(float x, double c2, double mc,
-                                           float& yh) {
-  const double y = fmax(__builtin_fma(static_cast<double>(x), c2, -mc), -256.0);
-  yh = static_cast<float>(y);
-  const float yl = static_cast<float>(y - static_cast<double>(yh));
-  const float e = __builtin_amdgcn_exp2f(yh);   // 0 below about -150
-  return __builtin_fmaf(e * static_cast<float>(kLn2d), yl, e);
+// The scale c2 = log2(e)/T: in fp64 for the state arithmetic, and as an
+// fp32 head c2h plus tail c2l for the per-logit terms (set once per kernel).
+struct ExpScale {
+  double c2;
+  float c2h, c2l;
+};
+
+__device__ __forceinline__ ExpScale exp_scale(double c2) {
+  ExpScale sc;
+  sc.c2 = c2;
+  sc.c2h = static_cast<float>(c2);
+  sc.c2l = static_cast<float>(c2 - static_cast<double>(sc.c2h));
+  return sc;
+}
+
+// Exponent constants of a state whose maximum is m: the split scale, and
+// m*c2h as an fp32 head mch plus its exact residual mcl (one fused
+// multiply-add), so that no rounding is shared by all the terms of a row.
+struct ExpConst {
+  float c2h, c2l, m, mch, mcl;
+};
+
+__device__ __forceinline__ ExpConst exp_const(float m, const ExpScale& sc) {
+  ExpConst k;
+  k.c2h = sc.c2h;
+  k.c2l = sc.c2l;
+  k.m = m;
+  k.mch = m * k.c2h;
+  k.mcl = __builtin_fmaf(m, k.c2h, -k.mch);
+  return k;
+}
+
+// One term of the sums: y = (x - m) * c2 in fp32, formed as
+// (x*c2h - mch, the product exact inside one fused multiply-add) - mcl
+// + (x - m)*c2l, clamped at -256 (a -inf logit, or an empty state's NaN,
+// gives 2^-256 = 0: never inf * 0), and 2^y.  What remains are the
+// roundings of these few operations, below |y| * 2^-22 relative in 2^y and
+// independent from term to term; with y near 0 for the terms that carry a
+// row's entropy above 1e-7, that is far inside the 1e-5 relative bar.
+__device__ __forceinline__ float exp2_term(float x, const ExpConst& k,
+                                           float& y) {
+  const float p = __builtin_fmaf(x, k.c2h, -k.mch);
+  y = fmaxf(__builtin_fmaf(x - k.m, k.c2l, p - k.mcl), -256.f);
+  return __builtin_amdgcn_exp2f(y);   // 0 below about -150
 }
 
 // Re-express state st relative to a larger maximum: every old term, the old
@@ -104,7 +138,9 @@ __device__ __forceinline__ State shfl_xor_state(const State& s, int mask) {
 // never summed, so nothing cancels later).
 template <int N>
 __device__ __forceinline__ void push_block(State& st, const float (&x)[N],
-                                           const int (&idx)[N], double c2) {
+                                           const int (&idx)[N],
+                                           const ExpScale& sc) {
+  const double c2 = sc.c2;
   float bm = x[0];
 #pragma unroll
   for (int k = 1; k < N; ++k) bm = fmaxf(bm, x[k]);
@@ -116,13 +152,13 @@ __device__ __forceinline__ void push_block(State& st, const float (&x)[N],
     for (int k = N - 1; k >= 0; --k) t = (x[k] == bm) ? idx[k] : t;
     st.tok = t;
   }
-  const double mc = static_cast<double>(st.m) * c2;
+  const ExpConst kc = exp_const(st.m, sc);
   float r = 0.f, sy = 0.f;
   int ties = 0;
 #pragma unroll
   for (int k = 0; k < N; ++k) {
     float yh;
-    float e = exp2_term(x[k], c2, mc, yh);
+    float e = exp2_term(x[k], kc, yh);
     const bool is_max = x[k] == st.m;
     e = is_max ? 0.f : e;
     ties += is_max ? 1 : 0;
