@@ -7,10 +7,15 @@
 // Work decomposition (persistent, balanced):
 //   grid      = n_rg row groups x n_slot slots, sized from the occupancy so
 //               that every workgroup is resident at once
-//   wave      = stream j = slot*8 + wave of its row group; it owns the
-//               contiguous vocabulary range [j*V/S, (j+1)*V/S) (S = 8 n_slot
-//               streams), so ranges differ by at most one row, and walks it
-//               in 32-row blocks, keeping a running score state per row
+//   waves     = VW vocabulary waves x RW row waves (VW * RW = 8); vocabulary
+//               wave v is stream j = slot*VW + v of its row group, which owns
+//               the contiguous vocabulary range [j*V/S, (j+1)*V/S) (S = VW
+//               n_slot streams), so ranges differ by at most one row; it
+//               walks the range in 32-row blocks.  The RW row waves of a
+//               stream take NB 32-row blocks of hidden rows each (a row
+//               group is 32*NB*RW rows), read the same weights (fetched once
+//               per CU, then from L1) and keep a running score state per row
+//               (RW is 2 for 129..512 rows, else 1)
 //   MFMA      = v_mfma_f32_32x32x16_bf16 computing logits^T: A = 32 weight
 //               rows x 16 k (registers), B = 16 k x 32 hidden rows (LDS)
 //   k order   = the contraction runs over k in a permuted order that is the
@@ -63,11 +68,16 @@ __device__ __forceinline__ int h_off(int r, int c) {
   return r * (kKStep * 2) + ((c ^ (r & 7)) << 4);
 }
 
-template <int NB>
+// NB 32-row blocks of hidden rows per wave, RW row waves, HPF register
+// stages of hidden rows (a divisor of kPF)
+template <int NB, int RW, int HPF>
 __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
-  constexpr int RG = 32 * NB;                       // hidden rows per group
+  constexpr int VW = kWaves / RW;                   // vocabulary waves
+  constexpr int RB = 32 * NB;                       // hidden rows per wave
+  constexpr int RG = RB * RW;                       // hidden rows per group
+  static_assert(kWaves % RW == 0 && kPF % HPF == 0, "wave and stage split");
   constexpr int kStage = RG * kKStep * 2;           // LDS bytes per step
-  constexpr int kRed = kWaves * RG * sizeof(State); // epilogue states
+  constexpr int kRed = kWaves * RB * sizeof(State); // epilogue states
   constexpr int kLds = 2 * kStage > kRed ? 2 * kStage : kRed;
   __shared__ __attribute__((aligned(16))) char smem[kLds];
 
@@ -78,12 +88,14 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   if (slot >= a.n_slot) return;
 
   const int wave = threadIdx.x / kWave;
+  const int vw = wave % VW;
+  const int rw = wave / VW;
   const int lane = lane_id();
   const int col = lane & 31;
   const int hf = lane >> 5;
   const int row0 = rg * RG;                         // first hidden row
-  const int64_t S = static_cast<int64_t>(a.n_slot) * kWaves;
-  const int64_t j = static_cast<int64_t>(slot) * kWaves + wave;
+  const int64_t S = static_cast<int64_t>(a.n_slot) * VW;
+  const int64_t j = static_cast<int64_t>(slot) * VW + vw;
   const int v_lo = static_cast<int>(j * a.V / S);
   const int v_hi = static_cast<int>((j + 1) * a.V / S);
   const int nsteps = a.Hd / kKStep;                 // a multiple of kPF
@@ -127,9 +139,9 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
     h_src[u] = hr * a.Hd + c * 8;        // element offset within step 0
     h_dst[u] = h_off(r, c);
   }
-  // a ring of kPF register stages: step s's rows live in stage s % kPF,
-  // loaded kPF steps before they go to LDS (L2 latency hidden)
-  u16x8_t hreg[kPF][kCPT];
+  // a ring of HPF register stages: step s's rows live in stage s % HPF,
+  // loaded HPF steps before they go to LDS (L2 latency hidden)
+  u16x8_t hreg[HPF][kCPT];
   auto hload = [&](int s, u16x8_t (&r)[kCPT]) {
 #pragma unroll
     for (int u = 0; u < kCPT; ++u)
@@ -141,7 +153,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
     for (int u = 0; u < kCPT; ++u)
       *reinterpret_cast<u16x8_t*>(sb + h_dst[u]) = r[u];
   };
-  auto hstep = [&](int s) { return s % nsteps; };
+  auto hstep = [&](int s) { return ((s % nsteps) + nsteps) % nsteps; };
 
   floatx16_t acc[NB];
   auto zero_acc = [&]() {
@@ -156,26 +168,28 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   for (int b = 0; b < NB; ++b) st[b] = empty_state();
   const ExpScale sc = exp_scale(a.c2);
 
-  // prologue: hidden step 0 into LDS, then the loads of four steps issued
-  // in the steady-state order (weights of step p, then hidden step p+1 into
-  // stage (p+1) % PF), so the loop head sees the same loads in flight from
-  // both of its predecessors and the compiler's waits stay partial
+  // prologue: hidden step 0 into LDS, then the loads of the PF steps before
+  // step 0 issued as those steps would (weights of step p, then hidden step
+  // p - PF + 1 + HPF into its stage; steps before 0 wrap and are never
+  // used), so the loop head sees the same loads in flight from both of its
+  // predecessors and the compiler's waits stay partial
   hload(0, hreg[0]);
   hstore(smem, hreg[0]);
 #pragma unroll
   for (int p = 0; p < kPF; ++p) {
     wload(p, wa[p]);
-    hload(hstep(p + 1), hreg[(p + 1) % kPF]);
+    const int hs = p - kPF + 1 + HPF;
+    hload(hstep(hs), hreg[((hs % HPF) + HPF) % HPF]);
   }
   __syncthreads();
 
   // step q = bi*nsteps + s (u = s % kPF, static): B fragments from LDS
   // buffer s&1 (nsteps is even), A from register stage u; then the stage is
-  // refilled with step q+PF, hidden step s+1 (register stage u+1) goes to
-  // the other LDS buffer and that stage is refilled with step s+1+PF
-  // (unconditionally: past the last step these are re-reads nobody uses).
-  // One barrier per step: the buffer written in step q was last read in
-  // step q-1, before its barrier.
+  // refilled with step q+PF, hidden step s+1 (register stage (u+1) % HPF)
+  // goes to the other LDS buffer and that stage is refilled with step
+  // s+1+HPF (unconditionally: past the last step these are re-reads nobody
+  // uses).  One barrier per step: the buffer written in step q was last
+  // read in step q-1, before its barrier.
   auto step = [&](const int u, const int q, const int s)
       __attribute__((always_inline)) {
     const char* sb = smem + (u & 1) * kStage;
@@ -186,7 +200,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
       for (int b = 0; b < NB; ++b)
         bfr[kk][b] = __builtin_bit_cast(
             bf16x8_t, *reinterpret_cast<const u16x8_t*>(
-                          sb + h_off(b * 32 + col, hf * 4 + kk)));
+                          sb + h_off(rw * RB + b * 32 + col, hf * 4 + kk)));
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const bf16x8_t af = __builtin_bit_cast(bf16x8_t, wa[u][kk]);
@@ -196,8 +210,8 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
                                                          acc[b], 0, 0, 0);
     }
     wload(q + kPF, wa[u]);
-    hstore(smem + ((u + 1) & 1) * kStage, hreg[(u + 1) % kPF]);
-    hload(hstep(s + 1 + kPF), hreg[(u + 1) % kPF]);
+    hstore(smem + ((u + 1) & 1) * kStage, hreg[(u + 1) % HPF]);
+    hload(hstep(s + 1 + HPF), hreg[(u + 1) % HPF]);
     __syncthreads();
   };
 
@@ -208,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
         step(u, bi * nsteps + s0 + u, s0 + u);
     }
     // block done: lane (col, hf) of row block b holds logits of hidden row
-    // row0 + 32b + col at vocabulary rows v0 + 8*(e/4) + 4*hf + e%4
+    // row0 + RB*rw + 32b + col at vocabulary rows v0 + 8*(e/4) + 4*hf + e%4
     const int v0 = v_lo + 32 * bi;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -225,18 +239,20 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
     zero_acc();
   }
 
-  // ---- the waves' states: both lane halves, then the eight waves in LDS
-  State* red = reinterpret_cast<State*>(smem);       // [kWaves][RG]
+  // ---- the waves' states: both lane halves, then the VW vocabulary waves
+  // of each row wave in LDS
+  State* red = reinterpret_cast<State*>(smem);       // [kWaves][RB]
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
     merge(st[b], shfl_xor_state(st[b], 32), a.c2);
-    if (hf == 0) red[wave * RG + b * 32 + col] = st[b];
+    if (hf == 0) red[wave * RB + b * 32 + col] = st[b];
   }
   __syncthreads();
   if (threadIdx.x < RG) {
     const int r = threadIdx.x;
-    State m = red[r];
-    for (int w = 1; w < kWaves; ++w) merge(m, red[w * RG + r], a.c2);
+    const int r_w = r / RB, r_l = r % RB;            // row wave, its row
+    State m = red[(r_w * VW) * RB + r_l];
+    for (int v = 1; v < VW; ++v) merge(m, red[(r_w * VW + v) * RB + r_l], a.c2);
     const int row = row0 + r;
     if (row < a.R) {
       if (a.n_slot == 1) finish(m, row, a.argmax, a.entropy, a.pmax);
@@ -257,11 +273,20 @@ __global__ __launch_bounds__(kWave) void lm_head_merge_kernel(LmArgs a) {
   if (lane_id() == 0) finish(st, row, a.argmax, a.entropy, a.pmax);
 }
 
-// Rows per group: all R rows when R <= 128 (one pass over the weights),
-// else groups of 128.
-int blocks_per_wave(int R) {
-  const int nb = (R + 31) / 32;
-  return nb < 4 ? nb : 4;
+// Row groups: up to 128 rows, one row wave with 1..4 blocks (a 256 x R
+// tile); up to 512 rows, groups of 256 rows in two row waves of 4 blocks (a
+// 128 x 256 tile: the same bytes per MFMA, half as many passes over the
+// weights; measured 29% faster at 384 rows); beyond, groups of 128 rows
+// again (measured faster at 1024 rows).  Narrower vocabulary tiles (more
+// row waves) re-stream the hidden rows from L2 faster than it delivers them.
+struct Shape {
+  int nb, rw;
+};
+
+Shape group_shape(int R) {
+  if (R <= 128) return {(R + 31) / 32, 1};
+  if (R <= 512) return {4, 2};
+  return {4, 1};
 }
 
 // Hd a multiple of 4 k steps: the weight stages then line up with the steps
@@ -272,46 +297,54 @@ bool lm_shape_ok(int R, int Hd, int V) {
          static_cast<int64_t>(R) * Hd < (1ll << 31);
 }
 
-template <int NB>
+template <int NB, int RW, int HPF>
 int resident_per_cu() {
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &n, reinterpret_cast<const void*>(lm_head_kernel<NB>),
+          &n, reinterpret_cast<const void*>(lm_head_kernel<NB, RW, HPF>),
           kThreads, 0) != hipSuccess || n < 1)
     n = 1;
   return n;
 }
 
+// the kernel of each group shape; occupancy index 0..4
+constexpr int kShapes = 5;
+int shape_index(Shape s) { return s.rw == 1 ? s.nb - 1 : 4; }
+
 // Slots per row group: every workgroup resident at once (CUs x occupancy),
 // no more streams than 32-row blocks.  Cached per device.
 struct LmPlan {
-  int nb, n_rg, n_slot, nblk;
+  Shape sh;
+  int n_rg, n_slot, nblk;
 };
 
 bool lm_plan(int R, int Hd, int V, LmPlan* p) {
   if (!lm_shape_ok(R, Hd, V)) return false;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
-  static int cus[64], occ[64][5];
+  static int cus[64], occ[64][kShapes];
   if (cus[dev] == 0) {
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount,
                               dev) != hipSuccess || n < 1)
       return false;
-    occ[dev][1] = resident_per_cu<1>();
-    occ[dev][2] = resident_per_cu<2>();
-    occ[dev][3] = resident_per_cu<3>();
-    occ[dev][4] = resident_per_cu<4>();
+    occ[dev][0] = resident_per_cu<1, 1, kPF>();
+    occ[dev][1] = resident_per_cu<2, 1, kPF>();
+    occ[dev][2] = resident_per_cu<3, 1, kPF>();
+    occ[dev][3] = resident_per_cu<4, 1, kPF>();
+    occ[dev][4] = resident_per_cu<4, 2, 2>();
     cus[dev] = n;
   }
-  p->nb = blocks_per_wave(R);
-  p->n_rg = (R + 32 * p->nb - 1) / (32 * p->nb);
-  int n_slot = cus[dev] * occ[dev][p->nb] / p->n_rg;
-  const int by_blocks = (V + 32 * kWaves - 1) / (32 * kWaves);
+  p->sh = group_shape(R);
+  const int rg = 32 * p->sh.nb * p->sh.rw;
+  const int vw = kWaves / p->sh.rw;
+  p->n_rg = (R + rg - 1) / rg;
+  int n_slot = cus[dev] * occ[dev][shape_index(p->sh)] / p->n_rg;
+  const int by_blocks = (V + 32 * vw - 1) / (32 * vw);
   if (n_slot > by_blocks) n_slot = by_blocks;
   if (n_slot < 1) n_slot = 1;
   p->n_slot = n_slot;
-  const int64_t S = static_cast<int64_t>(n_slot) * kWaves;
+  const int64_t S = static_cast<int64_t>(n_slot) * vw;
   const int64_t per = (V + S - 1) / S;               // rows of the longest
   p->nblk = static_cast<int>((per + 31) / 32);
   return true;
@@ -351,11 +384,12 @@ extern "C" int wedlm_lm_head_score(const uint16_t* hidden,
   // row group covers every slot
   const int64_t grid = 8ll * p.n_rg * ((p.n_slot + 7) / 8);
   if (grid > (1ll << 30)) return WEDLM_E_SHAPE;
-  switch (p.nb) {
-    case 1: hipLaunchKernelGGL(lm_head_kernel<1>, dim3(grid), dim3(kThreads), 0, st, a); break;
-    case 2: hipLaunchKernelGGL(lm_head_kernel<2>, dim3(grid), dim3(kThreads), 0, st, a); break;
-    case 3: hipLaunchKernelGGL(lm_head_kernel<3>, dim3(grid), dim3(kThreads), 0, st, a); break;
-    default: hipLaunchKernelGGL(lm_head_kernel<4>, dim3(grid), dim3(kThreads), 0, st, a); break;
+  switch (shape_index(p.sh)) {
+    case 0: hipLaunchKernelGGL((lm_head_kernel<1, 1, kPF>), dim3(grid), dim3(kThreads), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((lm_head_kernel<2, 1, kPF>), dim3(grid), dim3(kThreads), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((lm_head_kernel<3, 1, kPF>), dim3(grid), dim3(kThreads), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((lm_head_kernel<4, 1, kPF>), dim3(grid), dim3(kThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL((lm_head_kernel<4, 2, 2>), dim3(grid), dim3(kThreads), 0, st, a); break;
   }
   WEDLM_LAUNCH_CHECK();
   if (p.n_slot > 1) {

@@ -59,7 +59,9 @@ EXACT = [
     (40, 512, 513),      # two row blocks, ragged rows
     (96, 256, 2047),     # three row blocks
     (128, 512, 3001),    # four row blocks
-    (200, 768, 1500),    # two row groups (128 + 72)
+    (200, 768, 1500),    # one 256-row group in two row waves
+    (300, 512, 2000),    # two 256-row groups, the second ragged
+    (800, 256, 777),     # seven 128-row groups, the last ragged
     (17, 1024, 40000),   # several 32-row blocks per stream
 ]
 
