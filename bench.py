@@ -162,7 +162,6 @@ def bench_lm_head(args, dev):
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / n * 1e3
         flops = 2.0 * R * Hd * V
-        groups = -(-R // 128)
         w_bytes = V * Hd * 2
         alg_bytes = w_bytes + R * Hd * 2 + R * 12
         tflops = flops / us / 1e6
@@ -178,7 +177,7 @@ def bench_lm_head(args, dev):
         print(json.dumps({
             "kind": "lm_head_score", "R": R, "Hd": Hd, "V": V,
             "temperature": T, "us": us, "tflops": tflops,
-            "weight_gbps": w_bytes / us / 1e3, "row_groups": groups,
+            "weight_gbps": w_bytes / us / 1e3,
             "alg_bytes": alg_bytes, "flops": flops, "roofline": roof}),
             flush=True)
 

@@ -20,14 +20,16 @@
 //               rows x 16 k (registers), B = 16 k x 32 hidden rows (LDS)
 //   k order   = the contraction runs over k in a permuted order that is the
 //               same for A and B: in each 64-wide k step, lane half hf of
-//               MFMA j takes k = 32*hf + 8*j .. +8.  Each lane's A operand
-//               for a whole step is then 64 contiguous bytes of its weight
-//               row (four 16-byte loads), the B operand 16 contiguous bytes
-//               of an LDS row.
+//               MFMA j takes k = 32*hf + 8*j .. +8, i.e. 16-byte chunk
+//               4*hf + j of a 128-byte LDS row, for both operands.
 // Memory path: the weights are the HBM stream (V * Hd * 2 bytes per row
-//   group); each wave streams its own rows straight into registers, PF steps
-//   ahead, across block boundaries.  The hidden rows of a step go through
-//   LDS (XOR-swizzled 16-byte chunks), double-buffered, one barrier per step.
+//   group).  A stream's 32 rows of a k step (4 KB) are loaded coalesced,
+//   eight full 128-byte rows per wave instruction, split over its row waves,
+//   PF steps ahead across block boundaries, and go through a double-buffered
+//   LDS tile of the stream (a pattern with one row per lane touches 32 lines
+//   per instruction and streams about 25% slower).  The hidden rows of a
+//   step go through LDS the same way.  All LDS rows are XOR-swizzled 16-byte
+//   chunks; one barrier per step orders every buffer.
 //   Slots are placed so that the row groups of one slot share an XCD (and
 //   the weights they stream in its L2).
 // Epilogue: after each block a lane holds 16 logits of one hidden row per
@@ -69,16 +71,23 @@ __device__ __forceinline__ int h_off(int r, int c) {
 }
 
 // NB 32-row blocks of hidden rows per wave, RW row waves, HPF register
-// stages of hidden rows (a divisor of kPF)
-template <int NB, int RW, int HPF>
+// stages of hidden rows (a divisor of kPF); NT: weight loads carry the
+// non-temporal hint (one row group: nothing else reads the lines; with
+// several, the groups share them through L2 and the hint costs 5%)
+template <int NB, int RW, int HPF, bool NT>
 __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   constexpr int VW = kWaves / RW;                   // vocabulary waves
   constexpr int RB = 32 * NB;                       // hidden rows per wave
   constexpr int RG = RB * RW;                       // hidden rows per group
-  static_assert(kWaves % RW == 0 && kPF % HPF == 0, "wave and stage split");
-  constexpr int kStage = RG * kKStep * 2;           // LDS bytes per step
+  constexpr int NJ = 4 / RW;                        // weight loads per wave
+  static_assert(kWaves % RW == 0 && 4 % RW == 0 && kPF % HPF == 0,
+                "wave and stage split");
+  constexpr int kStage = RG * kKStep * 2;           // hidden LDS per step
+  constexpr int kWTile = 32 * kKStep * 2;           // weight LDS per step
+  constexpr int kWBase = 2 * kStage;                // weight tiles after
   constexpr int kRed = kWaves * RB * sizeof(State); // epilogue states
-  constexpr int kLds = 2 * kStage > kRed ? 2 * kStage : kRed;
+  constexpr int kMain = kWBase + VW * 2 * kWTile;
+  constexpr int kLds = kMain > kRed ? kMain : kRed;
   __shared__ __attribute__((aligned(16))) char smem[kLds];
 
   const int xcd = blockIdx.x % 8;
@@ -102,25 +111,37 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   const int nblk = a.nblk;
   const int total = nblk * nsteps;
 
-  // ---- weights: in block bi the lane streams row v_lo + 32 bi + col, bytes
-  // 64*hf .. 64*hf+63 of each 128-byte k step.  Every load is issued (no
-  // branch in the step, so the compiler's waits stay partial): a row past
-  // the stream's range re-reads its last row (a line another lane loads
-  // anyway) and its logits are masked; steps past the end re-read the last.
-  const uint16_t* wbase = a.w + hf * 32;
+  // ---- weights: the stream's 32 rows x 128 bytes of a k step are four
+  // 1 KB loads (8 rows each, lane l: row l/8 + 8j, chunk l%8); row wave rw
+  // issues loads j = rw, rw+RW, ...  Every load is issued (no branch in the
+  // step, so the compiler's waits stay partial): a row past the stream's
+  // range re-reads its last row and its logits are masked; steps past the
+  // end re-read the last.
   const int v_last = max(v_hi - 1, 0);
-  u16x8_t wa[kPF][4];
-  auto wload = [&](int q, u16x8_t (&r)[4]) {
+  const int w_row = lane >> 3, w_chunk = lane & 7;
+  char* const wtile = smem + kWBase + vw * 2 * kWTile;   // [2][32 x 128 B]
+  u16x8_t wa[kPF][NJ];
+  auto wload = [&](int q, u16x8_t (&r)[NJ]) {
     q = min(q, total - 1);
     const int bi = q / nsteps;
     const int s = q - bi * nsteps;
-    const int v = min(v_lo + 32 * bi + col, v_last);
-    const uint16_t* p = wbase + static_cast<int64_t>(v) * a.Hd + s * kKStep;
-    // plain loads: the four loads of a step share each 128-byte line, and
-    // a non-temporal hint would fetch the line once per load
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      r[u] = *reinterpret_cast<const u16x8_t*>(p + u * 8);
+    for (int i = 0; i < NJ; ++i) {
+      const int rr = w_row + 8 * (rw + i * RW);
+      const int v = min(v_lo + 32 * bi + rr, v_last);
+      const u16x8_t* p = reinterpret_cast<const u16x8_t*>(
+          a.w + static_cast<int64_t>(v) * a.Hd + s * kKStep + w_chunk * 8);
+      if constexpr (NT)
+        r[i] = __builtin_nontemporal_load(p);
+      else
+        r[i] = *p;
+    }
+  };
+  auto wstore = [&](char* wb, const u16x8_t (&r)[NJ]) {
+#pragma unroll
+    for (int i = 0; i < NJ; ++i)
+      *reinterpret_cast<u16x8_t*>(wb + h_off(w_row + 8 * (rw + i * RW),
+                                             w_chunk)) = r[i];
   };
 
   // ---- hidden rows: thread t moves 16-byte chunks t, t+512, ... of the
@@ -168,31 +189,41 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   for (int b = 0; b < NB; ++b) st[b] = empty_state();
   const ExpScale sc = exp_scale(a.c2);
 
-  // prologue: hidden step 0 into LDS, then the loads of the PF steps before
-  // step 0 issued as those steps would (weights of step p, then hidden step
-  // p - PF + 1 + HPF into its stage; steps before 0 wrap and are never
-  // used), so the loop head sees the same loads in flight from both of its
-  // predecessors and the compiler's waits stay partial
+  // prologue: step 0's hidden rows and weights into LDS, then the loads of
+  // the PF steps before step 0 issued as those steps would (weights of step
+  // p+1 into stage (p+1) % PF, then hidden step p - PF + 1 + HPF into its
+  // stage; steps before 0 wrap and are never used), so the loop head sees
+  // the same loads in flight from both of its predecessors and the
+  // compiler's waits stay partial
   hload(0, hreg[0]);
+  wload(0, wa[0]);
   hstore(smem, hreg[0]);
+  wstore(wtile, wa[0]);
 #pragma unroll
   for (int p = 0; p < kPF; ++p) {
-    wload(p, wa[p]);
+    wload(p + 1, wa[(p + 1) % kPF]);
     const int hs = p - kPF + 1 + HPF;
     hload(hstep(hs), hreg[((hs % HPF) + HPF) % HPF]);
   }
   __syncthreads();
 
-  // step q = bi*nsteps + s (u = s % kPF, static): B fragments from LDS
-  // buffer s&1 (nsteps is even), A from register stage u; then the stage is
-  // refilled with step q+PF, hidden step s+1 (register stage (u+1) % HPF)
-  // goes to the other LDS buffer and that stage is refilled with step
-  // s+1+HPF (unconditionally: past the last step these are re-reads nobody
-  // uses).  One barrier per step: the buffer written in step q was last
-  // read in step q-1, before its barrier.
+  // step q = bi*nsteps + s (u = s % kPF, static): A and B fragments from
+  // the LDS buffers s&1 (nsteps is even); then step s+1's weights (register
+  // stage (u+1) % PF) and hidden rows (stage (u+1) % HPF) go to the other
+  // buffers and those stages are refilled with steps q+1+PF and s+1+HPF
+  // (unconditionally: past the last step these are re-reads nobody uses).
+  // One barrier per step: a buffer written in step q was last read in step
+  // q-1, before its barrier, and is read in step q+1, after this one.
   auto step = [&](const int u, const int q, const int s)
       __attribute__((always_inline)) {
     const char* sb = smem + (u & 1) * kStage;
+    const char* wb = wtile + (u & 1) * kWTile;
+    bf16x8_t afr[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      afr[kk] = __builtin_bit_cast(
+          bf16x8_t,
+          *reinterpret_cast<const u16x8_t*>(wb + h_off(col, hf * 4 + kk)));
     bf16x8_t bfr[4][NB];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
@@ -203,13 +234,13 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
                           sb + h_off(rw * RB + b * 32 + col, hf * 4 + kk)));
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      const bf16x8_t af = __builtin_bit_cast(bf16x8_t, wa[u][kk]);
 #pragma unroll
       for (int b = 0; b < NB; ++b)
-        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bfr[kk][b],
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(afr[kk], bfr[kk][b],
                                                          acc[b], 0, 0, 0);
     }
-    wload(q + kPF, wa[u]);
+    wstore(wtile + ((u + 1) & 1) * kWTile, wa[(u + 1) % kPF]);
+    wload(q + 1 + kPF, wa[(u + 1) % kPF]);
     hstore(smem + ((u + 1) & 1) * kStage, hreg[(u + 1) % HPF]);
     hload(hstep(s + 1 + HPF), hreg[(u + 1) % HPF]);
     __syncthreads();
@@ -301,7 +332,7 @@ template <int NB, int RW, int HPF>
 int resident_per_cu() {
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &n, reinterpret_cast<const void*>(lm_head_kernel<NB, RW, HPF>),
+          &n, reinterpret_cast<const void*>(lm_head_kernel<NB, RW, HPF, true>),
           kThreads, 0) != hipSuccess || n < 1)
     n = 1;
   return n;
@@ -330,8 +361,8 @@ bool lm_plan(int R, int Hd, int V, LmPlan* p) {
       return false;
     occ[dev][0] = resident_per_cu<1, 1, kPF>();
     occ[dev][1] = resident_per_cu<2, 1, kPF>();
-    occ[dev][2] = resident_per_cu<3, 1, kPF>();
-    occ[dev][3] = resident_per_cu<4, 1, kPF>();
+    occ[dev][2] = resident_per_cu<3, 1, 2>();
+    occ[dev][3] = resident_per_cu<4, 1, 2>();
     occ[dev][4] = resident_per_cu<4, 2, 2>();
     cus[dev] = n;
   }
@@ -348,6 +379,22 @@ bool lm_plan(int R, int Hd, int V, LmPlan* p) {
   const int64_t per = (V + S - 1) / S;               // rows of the longest
   p->nblk = static_cast<int>((per + 31) / 32);
   return true;
+}
+
+// groups of fewer than 128 rows only occur with R < 128: one group
+template <int NB, int RW, int HPF>
+void launch(bool nt, int64_t grid, hipStream_t st, const LmArgs& a) {
+  if constexpr (NB * RW < 4) {
+    hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, true>), dim3(grid),
+                       dim3(kThreads), 0, st, a);
+  } else {
+    if (nt)
+      hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, true>), dim3(grid),
+                         dim3(kThreads), 0, st, a);
+    else
+      hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, false>), dim3(grid),
+                         dim3(kThreads), 0, st, a);
+  }
 }
 
 }  // namespace
@@ -384,12 +431,13 @@ extern "C" int wedlm_lm_head_score(const uint16_t* hidden,
   // row group covers every slot
   const int64_t grid = 8ll * p.n_rg * ((p.n_slot + 7) / 8);
   if (grid > (1ll << 30)) return WEDLM_E_SHAPE;
+  const bool nt = p.n_rg == 1;
   switch (shape_index(p.sh)) {
-    case 0: hipLaunchKernelGGL((lm_head_kernel<1, 1, kPF>), dim3(grid), dim3(kThreads), 0, st, a); break;
-    case 1: hipLaunchKernelGGL((lm_head_kernel<2, 1, kPF>), dim3(grid), dim3(kThreads), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((lm_head_kernel<3, 1, kPF>), dim3(grid), dim3(kThreads), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((lm_head_kernel<4, 1, kPF>), dim3(grid), dim3(kThreads), 0, st, a); break;
-    default: hipLaunchKernelGGL((lm_head_kernel<4, 2, 2>), dim3(grid), dim3(kThreads), 0, st, a); break;
+    case 0: launch<1, 1, kPF>(nt, grid, st, a); break;
+    case 1: launch<2, 1, kPF>(nt, grid, st, a); break;
+    case 2: launch<3, 1, 2>(nt, grid, st, a); break;
+    case 3: launch<4, 1, 2>(nt, grid, st, a); break;
+    default: launch<4, 2, 2>(nt, grid, st, a); break;
   }
   WEDLM_LAUNCH_CHECK();
   if (p.n_slot > 1) {
