@@ -113,6 +113,7 @@ def rng_for(seed: int, cid: int, step: int, part: int) -> np.random.Generator:
 # parts of the seed key
 _P_PREFIX_LEN, _P_WINDOW, _P_QKV, _P_TABLE, _P_LOGITS, _P_POOL, _P_KV = range(7)
 _P_DECISION = 7
+_P_MODEL, _P_PROMPT = 8, 9
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -371,6 +372,83 @@ def lm_head_inputs(R: int, Hd: int, V: int, seed: int = 0,
         wt = (wb[t].astype(np.uint32) << 16).view(np.float32)
         h[r] += np.float32(spike) * wt / np.float32((wt.astype(np.float64) ** 2).sum())
     return f32_to_bf16_bits(h), wb
+
+
+# --------------------------------------------------------------------------
+# decoder weights around the step (a Qwen3-shaped backbone, random init)
+# --------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class ModelShape:
+    name: str
+    cid: int
+    L: int                   # decoder layers
+    Hd: int                  # hidden size
+    Hq: int
+    Hkv: int
+    D: int
+    I: int                   # MLP inner size
+    V: int
+    theta: float = 1e6
+    eps: float = 1e-6        # RMSNorm epsilon
+    mask_id: int = -1        # vocabulary row of [M]; -1: the last row
+
+    @property
+    def mask_row(self) -> int:
+        return self.V - 1 if self.mask_id < 0 else self.mask_id
+
+    @property
+    def qkv_rows(self) -> int:
+        return (self.Hq + 2 * self.Hkv) * self.D
+
+
+MODEL_SHAPES: Dict[str, ModelShape] = {
+    "tiny2": ModelShape("tiny2", 300, L=2, Hd=256, Hq=4, Hkv=2, D=64, I=512,
+                        V=1000),
+    "qwen3_8b": ModelShape("qwen3_8b", 301, L=36, Hd=4096, Hq=32, Hkv=8,
+                           D=128, I=12288, V=151936),
+}
+
+MODEL_TENSORS = ("embed", "attn_norm", "w_qkv", "q_norm", "k_norm", "w_o",
+                 "mlp_norm", "w_gate_up", "w_down", "final_norm", "lm_head")
+
+
+def model_tensor_shapes(ms: ModelShape, layers: Optional[int] = None):
+    L = ms.L if layers is None else layers
+    return {
+        "embed": (ms.V, ms.Hd), "attn_norm": (L, ms.Hd),
+        "w_qkv": (L, ms.qkv_rows, ms.Hd), "q_norm": (L, ms.D),
+        "k_norm": (L, ms.D), "w_o": (L, ms.Hd, ms.Hq * ms.D),
+        "mlp_norm": (L, ms.Hd), "w_gate_up": (L, 2 * ms.I, ms.Hd),
+        "w_down": (L, ms.Hd, ms.I), "final_norm": (ms.Hd,),
+        "lm_head": (ms.V, ms.Hd)}
+
+
+def model_weights(ms: ModelShape, seed: int = 0,
+                  layers: Optional[int] = None) -> Dict[str, np.ndarray]:
+    """Random weights of the decoder, bf16 bits.  Projections ~ N(0, 1/fan_in)
+    (activations keep unit scale), norm gains 1 + N(0, 0.1^2), embeddings
+    N(0, 1), output layer N(0, 1/Hd).  Layouts: every projection is [out,
+    in] (one row per output feature); w_gate_up holds the gate rows, then
+    the up rows."""
+    out = {}
+    for i, (name, shape) in enumerate(model_tensor_shapes(ms, layers).items()):
+        rng = rng_for(seed, ms.cid, i, _P_MODEL)
+        x = rng.standard_normal(shape, dtype=np.float32)
+        if name.endswith("norm"):
+            x = np.float32(1.0) + np.float32(0.1) * x
+        elif name != "embed":
+            x /= np.float32(np.sqrt(shape[-1]))
+        out[name] = f32_to_bf16_bits(x)
+    return out
+
+
+def model_prompt(ms: ModelShape, B: int, c: int, seed: int = 0) -> np.ndarray:
+    """Prompt token ids [B, c], uniform over the vocabulary minus [M]."""
+    rng = rng_for(seed, ms.cid, 0, _P_PROMPT)
+    t = rng.integers(0, ms.V - 1, size=(B, c)).astype(np.int32)
+    t[t >= ms.mask_row] += 1
+    return t
 
 
 def gather_prefix(k_cache: np.ndarray, v_cache: np.ndarray, bt: np.ndarray,
