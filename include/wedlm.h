@@ -109,6 +109,10 @@ enum {
  *   q_phys    [B, W, Hq, D] bf16   rotated queries, physical order
  *   k_phys    [B, W, Hkv, D] bf16  rotated keys, physical order
  *   v_phys    [B, W, Hkv, D] bf16  values, physical order (copied)
+ * qkv_in, q_phys, k_phys and v_phys may all be NULL: the call then writes
+ * perm, pos_ids, tok_phys and n_obs only (a decoder computes its own
+ * queries and keys in physical order); some but not all NULL is
+ * WEDLM_E_ARG.
  */
 int wedlm_reorder(const int32_t* win_tok, const int32_t* win_start,
                   const uint16_t* qkv_in, int32_t B, int32_t W, int32_t Hq,

@@ -22,6 +22,7 @@
 // into their cache slots (V transposed, per the page layout), 16 bytes of
 // one row and head at a time.
 #include "common.h"
+#include "wedlm_model.h"
 
 using namespace wedlm;
 
@@ -48,6 +49,9 @@ struct CommitArgs {
   uint8_t* selected;
   int32_t* status;
   int rule;               // WEDLM_RULE_*
+  int n_layers;           // caches to extend (one per decoder layer)
+  int64_t win_lstride;    // elements between layers of k_phys / v_phys
+  int64_t cache_lstride;  // elements between layers of k_cache / v_cache
 };
 
 #pragma clang fp contract(off)
@@ -164,7 +168,12 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
   const int DG = D / 8;
   const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
   const int total = n * Hkv * DG;
-  for (int e = threadIdx.x; e < total; e += kThreads) {
+  for (int e2 = threadIdx.x; e2 < total * a.n_layers; e2 += kThreads) {
+    const int l = e2 / total, e = e2 - l * total;
+    const uint16_t* k_phys = a.k_phys + l * a.win_lstride;
+    const uint16_t* v_phys = a.v_phys + l * a.win_lstride;
+    uint16_t* k_cache = a.k_cache + l * a.cache_lstride;
+    uint16_t* v_cache = a.v_cache + l * a.cache_lstride;
     // K: e = (j, h, dg), dg fastest
     {
       const int dg = e % DG;
@@ -175,9 +184,9 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
       const int64_t pg = bt[p / kPage];
       const int row = p % kPage;
       const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
-          a.k_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
+          k_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
       *reinterpret_cast<u16x8_t*>(
-          a.k_cache + ((pg * Hkv + h) * kPage + row) * D + dg * 8) = v;
+          k_cache + ((pg * Hkv + h) * kPage + row) * D + dg * 8) = v;
     }
     // V: e = (h, dg, j), j fastest
     {
@@ -189,8 +198,8 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
       const int64_t pg = bt[p / kPage];
       const int row = p % kPage;
       const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
-          a.v_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
-      uint16_t* dst = a.v_cache + ((pg * Hkv + h) * D + dg * 8) * kPage + row;
+          v_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
+      uint16_t* dst = v_cache + ((pg * Hkv + h) * D + dg * 8) * kPage + row;
 #pragma unroll
       for (int k = 0; k < 8; ++k) dst[k * kPage] = v[k];
     }
@@ -209,7 +218,7 @@ int commit_impl(int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
                 int32_t W, int32_t Hkv, int32_t D, int32_t* n_commit,
                 int32_t* committed_tok, int32_t* committed_slot,
                 uint8_t* selected, int32_t* status, int32_t rule,
-                void* stream) {
+                int32_t n_layers, void* stream) {
   if (!win_tok || !win_start || !argmax || !entropy || !k_phys || !v_phys ||
       !k_cache || !v_cache || !block_table || !n_commit || !committed_tok ||
       !committed_slot || !selected || !status)
@@ -219,6 +228,7 @@ int commit_impl(int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
   if (rule != WEDLM_RULE_STREAMING && rule != WEDLM_RULE_BLOCK &&
       rule != WEDLM_RULE_ONE_TOKEN)
     return WEDLM_E_ARG;
+  if (n_layers < 1) return WEDLM_E_SHAPE;
   if (B < 1 || B > (1 << 30) || W < 1 || W > WEDLM_MAX_WINDOW || Hkv < 1 ||
       (D != 64 && D != 128))
     return WEDLM_E_SHAPE;
@@ -232,6 +242,9 @@ int commit_impl(int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
   a.n_commit = n_commit; a.committed_tok = committed_tok;
   a.committed_slot = committed_slot; a.selected = selected; a.status = status;
   a.rule = rule;
+  a.n_layers = n_layers;
+  a.win_lstride = static_cast<int64_t>(B) * W * Hkv * D;
+  a.cache_lstride = num_pages * Hkv * kPage * D;
   hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), a);
   WEDLM_LAUNCH_CHECK();
@@ -254,7 +267,7 @@ extern "C" int wedlm_commit(int32_t* win_tok, int32_t* win_start,
                      v_phys, k_cache, v_cache, num_pages, block_table,
                      max_pages, B, W, Hkv, D, n_commit, committed_tok,
                      committed_slot, selected, status, WEDLM_RULE_STREAMING,
-                     stream);
+                     1, stream);
 }
 
 extern "C" int wedlm_commit_rule(
@@ -268,5 +281,20 @@ extern "C" int wedlm_commit_rule(
   return commit_impl(win_tok, win_start, argmax, entropy, tau, lambda, k_phys,
                      v_phys, k_cache, v_cache, num_pages, block_table,
                      max_pages, B, W, Hkv, D, n_commit, committed_tok,
-                     committed_slot, selected, status, rule, stream);
+                     committed_slot, selected, status, rule, 1, stream);
+}
+
+extern "C" int wedlm_commit_layers(
+    int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
+    const float* entropy, double tau, double lambda, const uint16_t* k_win,
+    const uint16_t* v_win, uint16_t* k_cache, uint16_t* v_cache,
+    int64_t num_pages, const int32_t* block_table, int32_t max_pages,
+    int32_t B, int32_t W, int32_t Hkv, int32_t D, int32_t n_layers,
+    int32_t* n_commit, int32_t* committed_tok, int32_t* committed_slot,
+    uint8_t* selected, int32_t* status, int32_t rule, void* stream) {
+  return commit_impl(win_tok, win_start, argmax, entropy, tau, lambda, k_win,
+                     v_win, k_cache, v_cache, num_pages, block_table,
+                     max_pages, B, W, Hkv, D, n_commit, committed_tok,
+                     committed_slot, selected, status, rule, n_layers,
+                     stream);
 }

@@ -1,0 +1,567 @@
+// The decoder around the step: embedding, RMSNorm, the projections (a
+// weight-streaming GEMM with fused epilogues), per-head RMSNorm + RoPE of
+// the queries and keys, and the L-layer forward that strings them together
+// with the window attention and the fused output layer.  WeDLM-8B keeps its
+// Qwen3-8B backbone (Sec. 6.1); the forward runs the whole window in the
+// physical order of Eq. (5)/(6), positions from Eq. (2).
+//
+// GEMM (gemm_kernel): out[t][n] = sum_k x[t][k] * w[n][k] for the window's
+// M = B*W rows.  At decode sizes the weights are the HBM stream and every
+// weight byte is used by all M rows, so a workgroup owns one 32-feature
+// block (two for SwiGLU: the gate block and the matching up block) and one
+// group of 32*NB rows, and its 8 waves split K: wave w walks its own run of
+// 64-wide k steps with every load in registers PF steps ahead, no LDS and no
+// barrier in the loop.  The 8 partial tiles are summed through LDS in a fixed
+// order (deterministic) and the epilogue writes bf16, adds into the fp32
+// residual stream, or applies silu(gate) * up.
+//   MFMA      = v_mfma_f32_32x32x16_bf16, A = weight rows (features), B =
+//               activation rows (tokens); lane l holds row l%32 and, in each
+//               64-wide k step, lane half hf of MFMA j takes k = 32hf + 8j
+//               .. +8 of both operands: 64 contiguous bytes per lane per step
+//               (four 16-byte loads that share two 128-byte lines).
+//   output    = lane l, element e: feature 8(e/4) + 4(l/32) + e%4, token l%32.
+#include <math.h>
+
+#include "common.h"
+#include "wedlm_model.h"
+
+using namespace wedlm;
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// embedding: x[t] = E[token], [M] -> the mask row; fp32 residual stream
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void embed_kernel(
+    const int32_t* __restrict__ tok, int mask_row, int V,
+    const uint16_t* __restrict__ table, int Hd, float* __restrict__ x) {
+  const int t = blockIdx.x;
+  int id = tok[t];
+  if (id < 0) id = mask_row;
+  if (id >= V) id = mask_row;           // an id outside the table: [M]
+  const u16x8_t* src =
+      reinterpret_cast<const u16x8_t*>(table + static_cast<int64_t>(id) * Hd);
+  float* dst = x + static_cast<int64_t>(t) * Hd;
+  for (int c = threadIdx.x; c < Hd / 8; c += blockDim.x) {
+    const u16x8_t v = src[c];
+    floatx4_t lo, hi;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo[e] = bf16_to_f32(v[e]);
+      hi[e] = bf16_to_f32(v[e + 4]);
+    }
+    *reinterpret_cast<floatx4_t*>(dst + c * 8) = lo;
+    *reinterpret_cast<floatx4_t*>(dst + c * 8 + 4) = hi;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// RMSNorm: y = bf16(x / sqrt(mean(x^2) + eps) * g), one workgroup per row
+// ---------------------------------------------------------------------------
+constexpr int kNormThreads = 256;
+
+__global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
+    const float* __restrict__ x, const uint16_t* __restrict__ g, int Hd,
+    float eps, uint16_t* __restrict__ y) {
+  const int t = blockIdx.x;
+  const float* row = x + static_cast<int64_t>(t) * Hd;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < Hd / 4; c += kNormThreads) {
+    const floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
+    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+  __shared__ float part[kNormThreads / kWave];
+  if (lane_id() == 0) part[threadIdx.x / kWave] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < kNormThreads / kWave; ++i) tot += part[i];
+  const float r = 1.0f / sqrtf(tot / static_cast<float>(Hd) + eps);
+  uint16_t* out = y + static_cast<int64_t>(t) * Hd;
+  for (int c = threadIdx.x; c < Hd / 4; c += kNormThreads) {
+    const floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
+    const u16x4_t gg = *reinterpret_cast<const u16x4_t*>(g + c * 4);
+    u16x4_t o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = f32_to_bf16(v[e] * r * bf16_to_f32(gg[e]));
+    *reinterpret_cast<u16x4_t*>(out + c * 4) = o;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// per-head RMSNorm of q and k, then RoPE at the row's logical position
+// (Eq. 2; "rotate half": dimension i pairs with i + D/2 at angle
+// pos * theta^(-2i/D), angles in fp64); v is copied.  One workgroup per row;
+// one item = 8 rotation pairs of one head (two 16-byte loads), the D/16
+// items of a head sit on consecutive lanes and reduce their sum of squares
+// with xor shuffles.
+// ---------------------------------------------------------------------------
+constexpr int kQkThreads = 256;
+constexpr int kMaxHalf = 64;
+
+__global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
+    const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ gq,
+    const uint16_t* __restrict__ gk, const int32_t* __restrict__ pos_ids,
+    int Hq, int Hkv, int D, double theta, float eps,
+    uint16_t* __restrict__ q_out, uint16_t* __restrict__ k_out,
+    uint16_t* __restrict__ v_out) {
+  const int t = blockIdx.x;
+  const int half = D / 2;
+  const int per_head = half / 8;                  // items of a head: 4 or 8
+  const int n_items = (Hq + Hkv) * per_head;
+  const int H = Hq + 2 * Hkv;
+  const uint16_t* x = qkv + static_cast<int64_t>(t) * H * D;
+  __shared__ double s_cos[kMaxHalf], s_sin[kMaxHalf];
+  if (threadIdx.x < half) {
+    const int j = threadIdx.x;
+    const double pos = static_cast<double>(pos_ids[t]);
+    const double omega = pow(theta, -2.0 * j / D);
+    double sn, cs;
+    sincos(pos * omega, &sn, &cs);
+    s_cos[j] = cs;
+    s_sin[j] = sn;
+  }
+  __syncthreads();
+  // n_items is a multiple of per_head and every round starts at a multiple
+  // of kQkThreads, so a head's items never straddle a round or a wave
+  for (int base = 0; base < n_items; base += kQkThreads) {
+    const int it = base + threadIdx.x;
+    const bool live = it < n_items;
+    const int head = live ? it / per_head : 0;
+    const int j0 = live ? (it - head * per_head) * 8 : 0;
+    u16x8_t lo8 = {}, hi8 = {};
+    if (live) {
+      lo8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0);
+      hi8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0 + half);
+    }
+    float a[8], b[8], ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      a[e] = bf16_to_f32(lo8[e]);
+      b[e] = bf16_to_f32(hi8[e]);
+      ss += a[e] * a[e] + b[e] * b[e];
+    }
+    for (int off = 1; off < per_head; off <<= 1) ss += __shfl_xor(ss, off);
+    if (!live) continue;
+    const float r = 1.0f / sqrtf(ss / static_cast<float>(D) + eps);
+    const uint16_t* g = head < Hq ? gq : gk;
+    u16x8_t olo, ohi;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const double na = a[e] * r * bf16_to_f32(g[j0 + e]);
+      const double nb = b[e] * r * bf16_to_f32(g[j0 + e + half]);
+      const double cs = s_cos[j0 + e], sn = s_sin[j0 + e];
+      olo[e] = f32_to_bf16(static_cast<float>(na * cs - nb * sn));
+      ohi[e] = f32_to_bf16(static_cast<float>(nb * cs + na * sn));
+    }
+    uint16_t* dst = head < Hq
+                        ? q_out + (static_cast<int64_t>(t) * Hq + head) * D
+                        : k_out + (static_cast<int64_t>(t) * Hkv + head - Hq) * D;
+    *reinterpret_cast<u16x8_t*>(dst + j0) = olo;
+    *reinterpret_cast<u16x8_t*>(dst + j0 + half) = ohi;
+  }
+  const u16x8_t* xv = reinterpret_cast<const u16x8_t*>(x + (Hq + Hkv) * D);
+  u16x8_t* dv =
+      reinterpret_cast<u16x8_t*>(v_out + static_cast<int64_t>(t) * Hkv * D);
+  for (int e = threadIdx.x; e < Hkv * D / 8; e += kQkThreads) dv[e] = xv[e];
+}
+
+// ---------------------------------------------------------------------------
+// GEMM
+// ---------------------------------------------------------------------------
+constexpr int kGWaves = 8;
+constexpr int kGThreads = kGWaves * kWave;
+constexpr int kKStep = 64;
+constexpr int kRedStride = 33;                    // LDS row of 32 tokens + 1
+
+enum Epi { kStoreBf16 = 0, kAddF32 = 1, kSwiglu = 2 };
+
+struct GemmArgs {
+  const uint16_t* x;      // [M, K] activations
+  const uint16_t* w;      // [rows, K] weights
+  void* out;              // [M, ldo]
+  int M, N, K, ldo;
+  int up_off;             // SwiGLU: first row of the up block
+  int n_nb, n_rg;         // 32-feature blocks, row groups
+};
+
+template <int NB, int NA, int PF, int EPI>
+__global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
+  constexpr int RB = 32 * NB;
+  constexpr int TPC = 2;                            // tiles per LDS round
+  constexpr int BPC = TPC / NA;                     // row blocks per round
+  static_assert(NB % BPC == 0 || NB < BPC, "row blocks per round");
+  __shared__ float red[kGWaves * TPC * 32 * kRedStride];
+
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int nb = xcd + 8 * (local / a.n_rg);
+  const int rg = local % a.n_rg;
+  if (nb >= a.n_nb) return;                         // whole workgroup
+
+  const int lane = lane_id();
+  // the wave index in a scalar register: the step range and every branch on
+  // it below are then uniform scalar branches
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int col = lane & 31, hf = lane >> 5;
+  const int S = a.K / kKStep;
+  const int s0 = wave * S / kGWaves, s1 = (wave + 1) * S / kGWaves;
+  const int n = s1 - s0;
+
+  floatx16_t acc[NA][NB];
+#pragma unroll
+  for (int i = 0; i < NA; ++i)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][b][e] = 0.f;
+
+  if (n > 0) {
+    const uint16_t* wrow[NA];
+#pragma unroll
+    for (int i = 0; i < NA; ++i)
+      wrow[i] = a.w + static_cast<int64_t>(nb * 32 + col + i * a.up_off) * a.K +
+                hf * 32 + s0 * kKStep;
+    const uint16_t* xrow[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int t = min(rg * RB + b * 32 + col, a.M - 1);
+      xrow[b] = a.x + static_cast<int64_t>(t) * a.K + hf * 32 + s0 * kKStep;
+    }
+    u16x8_t wa[PF][NA][4], xb[PF][NB][4];
+    // every load is issued (steps past the run re-read its last step), so
+    // the waits in the loop stay partial
+    auto load = [&](int q, u16x8_t (&ra)[NA][4], u16x8_t (&rb)[NB][4]) {
+      const int off = min(q, n - 1) * kKStep;
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          ra[i][u] = *reinterpret_cast<const u16x8_t*>(wrow[i] + off + u * 8);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          rb[b][u] = *reinterpret_cast<const u16x8_t*>(xrow[b] + off + u * 8);
+    };
+    auto mfma = [&](const u16x8_t (&ra)[NA][4], const u16x8_t (&rb)[NB][4]) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < NA; ++i)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            acc[i][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8_t, ra[i][j]),
+                __builtin_bit_cast(bf16x8_t, rb[b][j]), acc[i][b], 0, 0, 0);
+    };
+#pragma unroll
+    for (int p = 0; p < PF; ++p) load(p, wa[p], xb[p]);
+    // whole groups of PF steps with no branch inside; step q + u sits in
+    // stage u, so the last n % PF steps are in stages 0 .. n % PF - 1
+    int q = 0;
+    for (; q + PF <= n; q += PF) {
+#pragma unroll
+      for (int u = 0; u < PF; ++u) {
+        mfma(wa[u], xb[u]);
+        load(q + u + PF, wa[u], xb[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < PF - 1; ++u)
+      if (q + u < n) mfma(wa[u], xb[u]);
+  }
+
+  // sum the 8 waves' partial tiles in wave order, TPC tiles per round
+  constexpr int kRounds = (NA * NB + TPC - 1) / TPC;
+#pragma unroll
+  for (int rd = 0; rd < kRounds; ++rd) {
+    if (rd > 0) __syncthreads();
+#pragma unroll
+    for (int tt = 0; tt < TPC; ++tt) {
+      const int tile = rd * TPC + tt;               // = b * NA + i
+      if (tile >= NA * NB) break;
+      const int i = tile % NA, b = tile / NA;
+      float* dst = red + (wave * TPC + tt) * 32 * kRedStride;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int f = 8 * (e >> 2) + 4 * hf + (e & 3);
+        dst[f * kRedStride + col] = acc[i][b][e];
+      }
+    }
+    __syncthreads();
+    // thread -> (feature f, token t): 32 features x 16 tokens, twice
+    const int f = threadIdx.x & 31;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int tl = (threadIdx.x >> 5) + 16 * half;
+#pragma unroll
+      for (int bb = 0; bb < BPC; ++bb) {
+        const int tile0 = rd * TPC + bb * NA;
+        if (tile0 >= NA * NB) break;
+        const int b = tile0 / NA;
+        const int tok = rg * RB + b * 32 + tl;
+        float v[NA];
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+          float s = 0.f;
+#pragma unroll
+          for (int w = 0; w < kGWaves; ++w)
+            s += red[((w * TPC + bb * NA + i) * 32 + f) * kRedStride + tl];
+          v[i] = s;
+        }
+        if (tok >= a.M) continue;
+        const int64_t o = static_cast<int64_t>(tok) * a.ldo + nb * 32 + f;
+        if constexpr (EPI == kStoreBf16) {
+          static_cast<uint16_t*>(a.out)[o] = f32_to_bf16(v[0]);
+        } else if constexpr (EPI == kAddF32) {
+          static_cast<float*>(a.out)[o] += v[0];
+        } else {
+          const float g = v[0], u = v[NA - 1];
+          static_cast<uint16_t*>(a.out)[o] =
+              f32_to_bf16(g / (1.0f + expf(-g)) * u);
+        }
+      }
+    }
+  }
+}
+
+// rows per group: 32, 64, then 128 (64 for SwiGLU, two weight blocks)
+int gemm_nb(int M, bool swiglu) {
+  if (M <= 32) return 1;
+  if (M <= 64 || swiglu) return 2;
+  return 4;
+}
+
+template <int NB, int NA, int PF, int EPI>
+void gemm_launch(const GemmArgs& a, hipStream_t st) {
+  const int64_t grid = 8ll * a.n_rg * ((a.n_nb + 7) / 8);
+  hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI>), dim3(grid),
+                     dim3(kGThreads), 0, st, a);
+}
+
+bool gemm_shape_ok(int M, int N, int K) {
+  return M >= 1 && N >= 32 && N % 32 == 0 && K >= kKStep && K % kKStep == 0 &&
+         static_cast<int64_t>(M) * K < (1ll << 40) &&
+         static_cast<int64_t>(N) * K * 2 < (1ll << 40);
+}
+
+int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
+         int ldo, int epi, hipStream_t st) {
+  if (!x || !w || !out) return WEDLM_E_ARG;
+  if (epi != kStoreBf16 && epi != kAddF32 && epi != kSwiglu) return WEDLM_E_ARG;
+  if (!gemm_shape_ok(M, N, K) || ldo < N) return WEDLM_E_SHAPE;
+  GemmArgs a{};
+  a.x = x; a.w = w; a.out = out; a.M = M; a.N = N; a.K = K; a.ldo = ldo;
+  a.up_off = N;
+  const int nb = gemm_nb(M, epi == kSwiglu);
+  a.n_nb = N / 32;
+  a.n_rg = (M + 32 * nb - 1) / (32 * nb);
+  if (8ll * a.n_rg * ((a.n_nb + 7) / 8) > (1ll << 30)) return WEDLM_E_SHAPE;
+  if (epi == kSwiglu) {
+    if (nb == 1) gemm_launch<1, 2, 2, kSwiglu>(a, st);
+    else gemm_launch<2, 2, 2, kSwiglu>(a, st);
+  } else if (epi == kAddF32) {
+    if (nb == 1) gemm_launch<1, 1, 4, kAddF32>(a, st);
+    else if (nb == 2) gemm_launch<2, 1, 2, kAddF32>(a, st);
+    else gemm_launch<4, 1, 2, kAddF32>(a, st);
+  } else {
+    if (nb == 1) gemm_launch<1, 1, 4, kStoreBf16>(a, st);
+    else if (nb == 2) gemm_launch<2, 1, 2, kStoreBf16>(a, st);
+    else gemm_launch<4, 1, 2, kStoreBf16>(a, st);
+  }
+  WEDLM_LAUNCH_CHECK();
+  return WEDLM_OK;
+}
+
+bool config_ok(const wedlm_model_config* c) {
+  return c && c->n_layers >= 1 && c->hidden >= 256 && c->hidden % 256 == 0 &&
+         c->n_kv_heads >= 1 && c->n_heads % c->n_kv_heads == 0 &&
+         (c->head_dim == 64 || c->head_dim == 128) && c->inter >= 32 &&
+         c->inter % 64 == 0 && c->vocab >= 1 && c->mask_token >= 0 &&
+         c->mask_token < c->vocab && c->rope_theta > 1.0 && c->rms_eps > 0.f &&
+         (static_cast<int64_t>(c->n_heads) * c->head_dim) % kKStep == 0;
+}
+
+// workspace carve-up of the forward, 256-byte aligned pieces
+struct Carve {
+  size_t x, xn, qkv, q, attn, act, attn_ws, lm_ws, total;
+};
+
+size_t up256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+Carve carve(const wedlm_model_config* c, int B, int W, int max_prefix_len) {
+  const size_t M = static_cast<size_t>(B) * W;
+  const size_t Hd = c->hidden, D = c->head_dim;
+  const size_t Hq = c->n_heads, Hkv = c->n_kv_heads;
+  Carve k{};
+  size_t off = 0;
+  k.x = off;    off += up256(M * Hd * 4);
+  k.xn = off;   off += up256(M * Hd * 2);
+  k.qkv = off;  off += up256(M * (Hq + 2 * Hkv) * D * 2);
+  k.q = off;    off += up256(M * Hq * D * 2);
+  k.attn = off; off += up256(M * Hq * D * 2);
+  k.act = off;  off += up256(M * c->inter * 2);
+  k.attn_ws = off;
+  off += up256(wedlm_window_attn_workspace_size(B, W, c->n_heads,
+                                                c->n_kv_heads, c->head_dim,
+                                                max_prefix_len));
+  k.lm_ws = off;
+  off += up256(wedlm_lm_head_score_workspace_size(static_cast<int32_t>(M),
+                                                  c->hidden, c->vocab));
+  k.total = off;
+  return k;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+
+extern "C" int wedlm_embed(const int32_t* tok, int32_t M, int32_t mask_token,
+                           const uint16_t* table, int32_t V, int32_t Hd,
+                           float* x, void* stream) {
+  if (!tok || !table || !x) return WEDLM_E_ARG;
+  if (M < 1 || V < 1 || mask_token < 0 || mask_token >= V || Hd < 8 ||
+      Hd % 8 != 0)
+    return WEDLM_E_SHAPE;
+  hipLaunchKernelGGL(embed_kernel, dim3(M), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), tok, mask_token, V,
+                     table, Hd, x);
+  WEDLM_LAUNCH_CHECK();
+  return WEDLM_OK;
+}
+
+extern "C" int wedlm_rmsnorm(const float* x, const uint16_t* gain, int32_t M,
+                             int32_t Hd, float eps, uint16_t* y,
+                             void* stream) {
+  if (!x || !gain || !y || !(eps > 0.f)) return WEDLM_E_ARG;
+  if (M < 1 || Hd < 4 || Hd % 4 != 0) return WEDLM_E_SHAPE;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(kNormThreads), 0,
+                     static_cast<hipStream_t>(stream), x, gain, Hd, eps, y);
+  WEDLM_LAUNCH_CHECK();
+  return WEDLM_OK;
+}
+
+extern "C" int wedlm_linear(const uint16_t* x, const uint16_t* w, int32_t M,
+                            int32_t N, int32_t K, int32_t epilogue, void* out,
+                            int32_t ldo, void* stream) {
+  return gemm(x, w, M, N, K, out, ldo, epilogue,
+              static_cast<hipStream_t>(stream));
+}
+
+extern "C" int wedlm_qk_norm_rope(const uint16_t* qkv, const uint16_t* q_gain,
+                                  const uint16_t* k_gain,
+                                  const int32_t* pos_ids, int32_t M,
+                                  int32_t Hq, int32_t Hkv, int32_t D,
+                                  double rope_theta, float eps,
+                                  uint16_t* q_out, uint16_t* k_out,
+                                  uint16_t* v_out, void* stream) {
+  if (!qkv || !q_gain || !k_gain || !pos_ids || !q_out || !k_out || !v_out)
+    return WEDLM_E_ARG;
+  if (!(rope_theta > 1.0) || !(eps > 0.f)) return WEDLM_E_ARG;
+  if (M < 1 || Hq < 1 || Hkv < 1 || (D != 64 && D != 128)) return WEDLM_E_SHAPE;
+  hipLaunchKernelGGL(qk_norm_rope_kernel, dim3(M), dim3(kQkThreads), 0,
+                     static_cast<hipStream_t>(stream), qkv, q_gain, k_gain,
+                     pos_ids, Hq, Hkv, D, rope_theta, eps, q_out, k_out,
+                     v_out);
+  WEDLM_LAUNCH_CHECK();
+  return WEDLM_OK;
+}
+
+extern "C" size_t wedlm_model_workspace_size(const wedlm_model_config* cfg,
+                                             int32_t B, int32_t W,
+                                             int32_t max_prefix_len) {
+  if (!config_ok(cfg) || B < 1 || W < 1 || W > WEDLM_MAX_WINDOW ||
+      max_prefix_len < 0)
+    return 0;
+  return carve(cfg, B, W, max_prefix_len).total;
+}
+
+extern "C" int wedlm_model_forward(
+    const wedlm_model_config* cfg, const wedlm_model_weights* wt,
+    const int32_t* win_tok, const int32_t* win_start, int32_t B, int32_t W,
+    const uint16_t* k_cache, const uint16_t* v_cache, int64_t num_pages,
+    const int32_t* block_table, int32_t max_pages, int32_t max_prefix_len,
+    double temperature, int32_t* perm, int32_t* pos_ids, int32_t* tok_phys,
+    int32_t* n_obs, uint16_t* k_win, uint16_t* v_win, int32_t* argmax,
+    float* entropy, float* pmax, int32_t* status, void* workspace,
+    size_t workspace_bytes, void* stream) {
+  if (!cfg || !wt || !win_tok || !win_start || !k_cache || !v_cache ||
+      !block_table || !perm || !pos_ids || !tok_phys || !n_obs || !k_win ||
+      !v_win || !argmax || !entropy || !status)
+    return WEDLM_E_ARG;
+  if (!wt->embed || !wt->attn_norm || !wt->w_qkv || !wt->q_norm ||
+      !wt->k_norm || !wt->w_o || !wt->mlp_norm || !wt->w_gate_up ||
+      !wt->w_down || !wt->final_norm || !wt->lm_head)
+    return WEDLM_E_ARG;
+  if (!(temperature > 0.0)) return WEDLM_E_ARG;
+  if (!config_ok(cfg) || B < 1 || W < 1 || W > WEDLM_MAX_WINDOW ||
+      max_prefix_len < 0 || num_pages < 1)
+    return WEDLM_E_SHAPE;
+  const Carve cv = carve(cfg, B, W, max_prefix_len);
+  if (!workspace || workspace_bytes < cv.total) return WEDLM_E_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  float* x = reinterpret_cast<float*>(ws + cv.x);
+  uint16_t* xn = reinterpret_cast<uint16_t*>(ws + cv.xn);
+  uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + cv.qkv);
+  uint16_t* q = reinterpret_cast<uint16_t*>(ws + cv.q);
+  uint16_t* attn = reinterpret_cast<uint16_t*>(ws + cv.attn);
+  uint16_t* act = reinterpret_cast<uint16_t*>(ws + cv.act);
+  void* attn_ws = ws + cv.attn_ws;
+  void* lm_ws = ws + cv.lm_ws;
+  const size_t attn_ws_bytes = cv.lm_ws - cv.attn_ws;
+  const size_t lm_ws_bytes = cv.total - cv.lm_ws;
+
+  const int M = B * W;
+  const int Hd = cfg->hidden, Hq = cfg->n_heads, Hkv = cfg->n_kv_heads;
+  const int D = cfg->head_dim, I = cfg->inter;
+  const int QKV = (Hq + 2 * Hkv) * D;
+  const int64_t win_stride = static_cast<int64_t>(M) * Hkv * D;
+  const int64_t cache_stride = num_pages * Hkv * kPage * D;
+  const float scale = 1.0f / sqrtf(static_cast<float>(D));
+  int rc;
+#define WEDLM_TRY(call) \
+  if ((rc = (call)) != WEDLM_OK) return rc
+
+  // physical order of the window (Eq. 5/6) and its positions (Eq. 2)
+  WEDLM_TRY(wedlm_reorder(win_tok, win_start, nullptr, B, W, Hq, Hkv, D,
+                          cfg->rope_theta, perm, pos_ids, tok_phys, n_obs,
+                          nullptr, nullptr, nullptr, stream));
+  WEDLM_TRY(wedlm_embed(tok_phys, M, cfg->mask_token, wt->embed, cfg->vocab,
+                        Hd, x, stream));
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    uint16_t* kl = k_win + l * win_stride;
+    uint16_t* vl = v_win + l * win_stride;
+    WEDLM_TRY(wedlm_rmsnorm(x, wt->attn_norm + static_cast<int64_t>(l) * Hd,
+                            M, Hd, cfg->rms_eps, xn, stream));
+    WEDLM_TRY(gemm(xn, wt->w_qkv + static_cast<int64_t>(l) * QKV * Hd, M, QKV,
+                   Hd, qkv, QKV, kStoreBf16, st));
+    WEDLM_TRY(wedlm_qk_norm_rope(qkv, wt->q_norm + static_cast<int64_t>(l) * D,
+                                 wt->k_norm + static_cast<int64_t>(l) * D,
+                                 pos_ids, M, Hq, Hkv, D, cfg->rope_theta,
+                                 cfg->rms_eps, q, kl, vl, stream));
+    WEDLM_TRY(wedlm_window_attn(
+        q, kl, vl, k_cache + l * cache_stride, v_cache + l * cache_stride,
+        num_pages, block_table, max_pages, win_start, B, W, Hq, Hkv, D,
+        max_prefix_len, scale, attn, nullptr, status, attn_ws, attn_ws_bytes,
+        stream));
+    WEDLM_TRY(gemm(attn, wt->w_o + static_cast<int64_t>(l) * Hd * Hq * D, M,
+                   Hd, Hq * D, x, Hd, kAddF32, st));
+    WEDLM_TRY(wedlm_rmsnorm(x, wt->mlp_norm + static_cast<int64_t>(l) * Hd, M,
+                            Hd, cfg->rms_eps, xn, stream));
+    WEDLM_TRY(gemm(xn, wt->w_gate_up + static_cast<int64_t>(l) * 2 * I * Hd, M,
+                   I, Hd, act, I, kSwiglu, st));
+    WEDLM_TRY(gemm(act, wt->w_down + static_cast<int64_t>(l) * Hd * I, M, Hd,
+                   I, x, Hd, kAddF32, st));
+  }
+  WEDLM_TRY(wedlm_rmsnorm(x, wt->final_norm, M, Hd, cfg->rms_eps, xn, stream));
+  WEDLM_TRY(wedlm_lm_head_score(xn, wt->lm_head, M, Hd, cfg->vocab,
+                                temperature, argmax, entropy, pmax, lm_ws,
+                                lm_ws_bytes, stream));
+#undef WEDLM_TRY
+  return WEDLM_OK;
+}

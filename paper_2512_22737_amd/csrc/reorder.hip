@@ -50,6 +50,7 @@ __global__ __launch_bounds__(kThreads) void reorder_rope_kernel(
     }
   }
   __syncthreads();
+  if (qkv_in == nullptr) return;                  // indices only (uniform)
   const int src = s_src;
   const int half = D / 2;
   const int H = Hq + 2 * Hkv;
@@ -117,9 +118,12 @@ extern "C" int wedlm_reorder(const int32_t* win_tok, const int32_t* win_start,
                              int32_t* n_obs, uint16_t* q_phys,
                              uint16_t* k_phys, uint16_t* v_phys,
                              void* stream) {
-  if (!win_tok || !win_start || !qkv_in || !perm || !pos_ids || !tok_phys ||
-      !n_obs || !q_phys || !k_phys || !v_phys)
+  if (!win_tok || !win_start || !perm || !pos_ids || !tok_phys || !n_obs)
     return WEDLM_E_ARG;
+  // the gather and rotation are all or nothing: without them the call
+  // computes the indices only
+  const int given = !!qkv_in + !!q_phys + !!k_phys + !!v_phys;
+  if (given != 0 && given != 4) return WEDLM_E_ARG;
   if (!(rope_theta > 1.0) || !(rope_theta < 1e300)) return WEDLM_E_ARG;
   if (B < 1 || B > 65535 || W < 1 || W > WEDLM_MAX_WINDOW || Hkv < 1 ||
       Hq < Hkv || Hq % Hkv != 0 || (D != 64 && D != 128) ||

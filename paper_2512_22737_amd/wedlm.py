@@ -1,4 +1,4 @@
-"""Thin Python binding of libwedlm.so (include/wedlm.h).
+"""Thin Python binding of libwedlm.so (include/wedlm.h, include/wedlm_model.h).
 
 Argument marshalling only: each function checks the tensors it is handed
 (device, dtype, contiguity, shape), reads the sizes off them and calls the C
@@ -69,6 +69,25 @@ def _load():
     lib.wedlm_lm_head_score.argtypes = [P, P, I32, I32, I32, D_, P, P, P, P,
                                         SZ, P]
     lib.wedlm_lm_head_score.restype = ctypes.c_int
+    lib.wedlm_embed.argtypes = [P, I32, I32, P, I32, I32, P, P]
+    lib.wedlm_embed.restype = ctypes.c_int
+    lib.wedlm_rmsnorm.argtypes = [P, P, I32, I32, F, P, P]
+    lib.wedlm_rmsnorm.restype = ctypes.c_int
+    lib.wedlm_linear.argtypes = [P, P, I32, I32, I32, I32, P, I32, P]
+    lib.wedlm_linear.restype = ctypes.c_int
+    lib.wedlm_qk_norm_rope.argtypes = [P, P, P, P, I32, I32, I32, I32, D_, F,
+                                       P, P, P, P]
+    lib.wedlm_qk_norm_rope.restype = ctypes.c_int
+    lib.wedlm_model_workspace_size.argtypes = [P, I32, I32, I32]
+    lib.wedlm_model_workspace_size.restype = SZ
+    lib.wedlm_model_forward.argtypes = [P, P, P, P, I32, I32, P, P, I64, P,
+                                        I32, I32, D_, P, P, P, P, P, P, P, P,
+                                        P, P, P, SZ, P]
+    lib.wedlm_model_forward.restype = ctypes.c_int
+    lib.wedlm_commit_layers.argtypes = [P, P, P, P, D_, D_, P, P, P, P, I64,
+                                        P, I32, I32, I32, I32, I32, I32, P, P,
+                                        P, P, P, I32, P]
+    lib.wedlm_commit_layers.restype = ctypes.c_int
     lib.wedlm_strerror.argtypes = [ctypes.c_int]
     lib.wedlm_strerror.restype = ctypes.c_char_p
     lib.wedlm_version.argtypes = []
@@ -85,7 +104,9 @@ EXPORTED = ["wedlm_reorder", "wedlm_window_attn_workspace_size",
             "wedlm_window_attn", "wedlm_score_workspace_size", "wedlm_score",
             "wedlm_commit", "wedlm_commit_rule",
             "wedlm_lm_head_score_workspace_size", "wedlm_lm_head_score",
-            "wedlm_strerror", "wedlm_version"]
+            "wedlm_strerror", "wedlm_version", "wedlm_embed", "wedlm_rmsnorm",
+            "wedlm_linear", "wedlm_qk_norm_rope", "wedlm_model_workspace_size",
+            "wedlm_model_forward", "wedlm_commit_layers"]
 
 # decoding rules of wedlm_commit_rule (include/wedlm.h)
 RULE_STREAMING, RULE_BLOCK, RULE_ONE_TOKEN = 0, 1, 2
@@ -132,20 +153,24 @@ def wedlm_strerror(code: int) -> str:
 
 def wedlm_reorder(win_tok, win_start, qkv_in, Hq: int, Hkv: int,
                   rope_theta: float, perm, pos_ids, tok_phys, n_obs, q_phys,
-                  k_phys, v_phys) -> None:
+                  k_phys, v_phys, D: Optional[int] = None) -> None:
+    """qkv_in, q_phys, k_phys, v_phys all None: indices only (D then sizes
+    the argument check alone)."""
     B, W = win_tok.shape
-    D = qkv_in.shape[-1]
+    none = qkv_in is None
+    D = (D or 128) if none else qkv_in.shape[-1]
     i32 = (torch.int32,)
     code = _load().wedlm_reorder(
         _t(win_tok, "win_tok", i32, (B, W)),
         _t(win_start, "win_start", i32, (B,)),
-        _t(qkv_in, "qkv_in", _BF16, (B, W, Hq + 2 * Hkv, D)),
+        _t(qkv_in, "qkv_in", _BF16, (B, W, Hq + 2 * Hkv, D), allow_none=none),
         B, W, Hq, Hkv, D, float(rope_theta),
         _t(perm, "perm", i32, (B, W)), _t(pos_ids, "pos_ids", i32, (B, W)),
         _t(tok_phys, "tok_phys", i32, (B, W)), _t(n_obs, "n_obs", i32, (B,)),
-        _t(q_phys, "q_phys", _BF16, (B, W, Hq, D)),
-        _t(k_phys, "k_phys", _BF16, (B, W, Hkv, D)),
-        _t(v_phys, "v_phys", _BF16, (B, W, Hkv, D)), _stream())
+        _t(q_phys, "q_phys", _BF16, (B, W, Hq, D), allow_none=none),
+        _t(k_phys, "k_phys", _BF16, (B, W, Hkv, D), allow_none=none),
+        _t(v_phys, "v_phys", _BF16, (B, W, Hkv, D), allow_none=none),
+        _stream())
     _check(code, "wedlm_reorder")
 
 
@@ -370,3 +395,229 @@ class DecodeStep:
         self.attn(k_cache, v_cache, block_table, win_start)
         self.score(logits)
         self.commit(win_tok, win_start, k_cache, v_cache, block_table)
+
+
+# ---------------------------------------------------------------------------
+# the decoder around the step (include/wedlm_model.h)
+# ---------------------------------------------------------------------------
+
+EPI_STORE_BF16, EPI_ADD_F32, EPI_SWIGLU = 0, 1, 2
+
+
+class ModelConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("inter", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("mask_token", ctypes.c_int32),
+                ("rope_theta", ctypes.c_double), ("rms_eps", ctypes.c_float)]
+
+
+WEIGHT_NAMES = ("embed", "attn_norm", "w_qkv", "q_norm", "k_norm", "w_o",
+                "mlp_norm", "w_gate_up", "w_down", "final_norm", "lm_head")
+
+
+class ModelWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_NAMES]
+
+
+def model_config(L, Hd, Hq, Hkv, D, I, V, mask_token, theta=1e6, eps=1e-6):
+    return ModelConfig(L, Hd, Hq, Hkv, D, I, V, mask_token, float(theta),
+                       float(eps))
+
+
+def weight_shapes(cfg: ModelConfig):
+    L, Hd, Hq, Hkv = cfg.n_layers, cfg.hidden, cfg.n_heads, cfg.n_kv_heads
+    D, I, V = cfg.head_dim, cfg.inter, cfg.vocab
+    return {"embed": (V, Hd), "attn_norm": (L, Hd),
+            "w_qkv": (L, (Hq + 2 * Hkv) * D, Hd), "q_norm": (L, D),
+            "k_norm": (L, D), "w_o": (L, Hd, Hq * D), "mlp_norm": (L, Hd),
+            "w_gate_up": (L, 2 * I, Hd), "w_down": (L, Hd, I),
+            "final_norm": (Hd,), "lm_head": (V, Hd)}
+
+
+def model_weights(cfg: ModelConfig, tensors: dict) -> ModelWeights:
+    """Check the weight tensors against the config and point the struct at
+    them (the caller keeps the tensors alive)."""
+    shapes = weight_shapes(cfg)
+    return ModelWeights(*[_t(tensors[n], n, _BF16, shapes[n])
+                          for n in WEIGHT_NAMES])
+
+
+def wedlm_embed(tok, mask_token: int, table, x) -> None:
+    M = tok.numel()
+    V, Hd = table.shape
+    code = _load().wedlm_embed(
+        _t(tok, "tok", (torch.int32,)), M, int(mask_token),
+        _t(table, "table", _BF16), V, Hd,
+        _t(x, "x", (torch.float32,), (M, Hd)), _stream())
+    _check(code, "wedlm_embed")
+
+
+def wedlm_rmsnorm(x, gain, eps: float, y) -> None:
+    M, Hd = x.shape
+    code = _load().wedlm_rmsnorm(
+        _t(x, "x", (torch.float32,)), _t(gain, "gain", _BF16, (Hd,)), M, Hd,
+        float(eps), _t(y, "y", _BF16, (M, Hd)), _stream())
+    _check(code, "wedlm_rmsnorm")
+
+
+def wedlm_linear(x, w, epilogue: int, out) -> None:
+    """out = x w^T with the epilogue of include/wedlm_model.h; x [M, K],
+    w [rows, K] (rows = 2N for SwiGLU), out [M, ldo] with ldo >= N."""
+    M, K = x.shape
+    rows = w.shape[0]
+    N = rows // 2 if epilogue == EPI_SWIGLU else rows
+    odt = (torch.float32,) if epilogue == EPI_ADD_F32 else _BF16
+    if out.dim() != 2 or out.shape[0] != M:
+        raise WedlmError(f"out: shape {tuple(out.shape)} is not [{M}, >= {N}]")
+    code = _load().wedlm_linear(
+        _t(x, "x", _BF16), _t(w, "w", _BF16, (rows, K)), M, N, K,
+        int(epilogue), _t(out, "out", odt), out.shape[1], _stream())
+    _check(code, "wedlm_linear")
+
+
+def wedlm_qk_norm_rope(qkv, q_gain, k_gain, pos_ids, Hq: int, Hkv: int,
+                       rope_theta: float, eps: float, q_out, k_out,
+                       v_out) -> None:
+    M = qkv.shape[0]
+    D = q_gain.shape[0]
+    i32 = (torch.int32,)
+    code = _load().wedlm_qk_norm_rope(
+        _t(qkv, "qkv", _BF16, (M, (Hq + 2 * Hkv) * D)),
+        _t(q_gain, "q_gain", _BF16, (D,)), _t(k_gain, "k_gain", _BF16, (D,)),
+        _t(pos_ids, "pos_ids", i32), M, Hq, Hkv, D, float(rope_theta),
+        float(eps), _t(q_out, "q_out", _BF16), _t(k_out, "k_out", _BF16),
+        _t(v_out, "v_out", _BF16), _stream())
+    _check(code, "wedlm_qk_norm_rope")
+
+
+def wedlm_model_workspace_size(cfg: ModelConfig, B: int, W: int,
+                               max_prefix_len: int) -> int:
+    return int(_load().wedlm_model_workspace_size(ctypes.byref(cfg), B, W,
+                                                  max_prefix_len))
+
+
+def wedlm_model_forward(cfg: ModelConfig, weights: ModelWeights, win_tok,
+                        win_start, k_cache, v_cache, block_table,
+                        max_prefix_len: int, temperature: float, perm,
+                        pos_ids, tok_phys, n_obs, k_win, v_win, argmax,
+                        entropy, pmax, status, workspace) -> None:
+    B, W = win_tok.shape
+    L, Hkv, D = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
+    P = k_cache.shape[1]
+    maxp = block_table.shape[1]
+    i32, f32 = (torch.int32,), (torch.float32,)
+    code = _load().wedlm_model_forward(
+        ctypes.byref(cfg), ctypes.byref(weights),
+        _t(win_tok, "win_tok", i32, (B, W)),
+        _t(win_start, "win_start", i32, (B,)), B, W,
+        _t(k_cache, "k_cache", _BF16, (L, P, Hkv, PAGE_SIZE, D)),
+        _t(v_cache, "v_cache", _BF16, (L, P, Hkv, D, PAGE_SIZE)), P,
+        _t(block_table, "block_table", i32, (B, maxp)), maxp,
+        int(max_prefix_len), float(temperature),
+        _t(perm, "perm", i32, (B, W)), _t(pos_ids, "pos_ids", i32, (B, W)),
+        _t(tok_phys, "tok_phys", i32, (B, W)), _t(n_obs, "n_obs", i32, (B,)),
+        _t(k_win, "k_win", _BF16, (L, B, W, Hkv, D)),
+        _t(v_win, "v_win", _BF16, (L, B, W, Hkv, D)),
+        _t(argmax, "argmax", i32, (B, W)), _t(entropy, "entropy", f32, (B, W)),
+        _t(pmax, "pmax", f32, (B, W), allow_none=True),
+        _t(status, "status", i32, (B,)), _t(workspace, "workspace",
+                                            (torch.uint8,)),
+        workspace.numel(), _stream())
+    _check(code, "wedlm_model_forward")
+
+
+def wedlm_commit_layers(win_tok, win_start, argmax, entropy, tau: float,
+                        lam: float, k_win, v_win, k_cache, v_cache,
+                        block_table, n_commit, committed_tok, committed_slot,
+                        selected, status, rule: int = RULE_STREAMING) -> None:
+    B, W = win_tok.shape
+    L, _, _, Hkv, D = k_win.shape
+    P = k_cache.shape[1]
+    maxp = block_table.shape[1]
+    i32 = (torch.int32,)
+    code = _load().wedlm_commit_layers(
+        _t(win_tok, "win_tok", i32, (B, W)),
+        _t(win_start, "win_start", i32, (B,)),
+        _t(argmax, "argmax", i32, (B, W)),
+        _t(entropy, "entropy", (torch.float32,), (B, W)), float(tau),
+        float(lam), _t(k_win, "k_win", _BF16, (L, B, W, Hkv, D)),
+        _t(v_win, "v_win", _BF16, (L, B, W, Hkv, D)),
+        _t(k_cache, "k_cache", _BF16, (L, P, Hkv, PAGE_SIZE, D)),
+        _t(v_cache, "v_cache", _BF16, (L, P, Hkv, D, PAGE_SIZE)), P,
+        _t(block_table, "block_table", i32, (B, maxp)), maxp, B, W, Hkv, D, L,
+        _t(n_commit, "n_commit", i32, (B,)),
+        _t(committed_tok, "committed_tok", i32, (B, W)),
+        _t(committed_slot, "committed_slot", i32, (B, W)),
+        _t(selected, "selected", (torch.uint8,), (B, W)),
+        _t(status, "status", i32, (B,)), int(rule), _stream())
+    _check(code, "wedlm_commit_layers")
+
+
+class Decoder:
+    """A decoder's device state for B sequences and the two calls of one
+    streaming step (wedlm_model_forward, wedlm_commit_layers).
+
+    weights: dict of bf16 device tensors (WEIGHT_NAMES, weight_shapes()).
+    Caches: [L, num_pages, ...]; each sequence owns the pages its block-table
+    row lists.  The window state (win_tok, win_start) lives here and is
+    updated in place by step()."""
+
+    def __init__(self, cfg: ModelConfig, weights: dict, B: int, W: int,
+                 num_pages: int, block_table, max_prefix_len: int,
+                 tau=0.9, lam=0.01, temperature=0.1, rule="stream",
+                 device="cuda"):
+        self.cfg, self.B, self.W = cfg, B, W
+        self.tensors = weights
+        self.weights = model_weights(cfg, weights)
+        self.tau, self.lam, self.temperature = tau, lam, temperature
+        self.rule = RULES[rule]
+        self.max_prefix_len = int(max_prefix_len)
+        dev = torch.device(device)
+        L, Hkv, D = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
+        i32 = dict(dtype=torch.int32, device=dev)
+        bf = dict(dtype=torch.bfloat16, device=dev)
+        self.k_cache = torch.zeros(L, num_pages, Hkv, PAGE_SIZE, D, **bf)
+        self.v_cache = torch.zeros(L, num_pages, Hkv, D, PAGE_SIZE, **bf)
+        self.block_table = block_table
+        self.win_tok = torch.full((B, W), MASK_TOKEN, **i32)
+        self.win_start = torch.zeros(B, **i32)
+        self.perm = torch.empty(B, W, **i32)
+        self.pos_ids = torch.empty(B, W, **i32)
+        self.tok_phys = torch.empty(B, W, **i32)
+        self.n_obs = torch.empty(B, **i32)
+        self.k_win = torch.empty(L, B, W, Hkv, D, **bf)
+        self.v_win = torch.empty(L, B, W, Hkv, D, **bf)
+        self.argmax = torch.empty(B, W, **i32)
+        self.entropy = torch.empty(B, W, dtype=torch.float32, device=dev)
+        self.pmax = torch.empty(B, W, dtype=torch.float32, device=dev)
+        self.attn_status = torch.zeros(B, **i32)
+        self.n_commit = torch.empty(B, **i32)
+        self.committed_tok = torch.empty(B, W, **i32)
+        self.committed_slot = torch.empty(B, W, **i32)
+        self.selected = torch.empty(B, W, dtype=torch.uint8, device=dev)
+        self.status = torch.zeros(B, **i32)
+        n = wedlm_model_workspace_size(cfg, B, W, self.max_prefix_len)
+        if n == 0:
+            raise WedlmError("invalid decoder configuration")
+        self.workspace = torch.empty(n, dtype=torch.uint8, device=dev)
+
+    def forward(self):
+        wedlm_model_forward(
+            self.cfg, self.weights, self.win_tok, self.win_start,
+            self.k_cache, self.v_cache, self.block_table,
+            self.max_prefix_len, self.temperature, self.perm, self.pos_ids,
+            self.tok_phys, self.n_obs, self.k_win, self.v_win, self.argmax,
+            self.entropy, self.pmax, self.attn_status, self.workspace)
+
+    def commit(self):
+        wedlm_commit_layers(
+            self.win_tok, self.win_start, self.argmax, self.entropy,
+            self.tau, self.lam, self.k_win, self.v_win, self.k_cache,
+            self.v_cache, self.block_table, self.n_commit,
+            self.committed_tok, self.committed_slot, self.selected,
+            self.status, self.rule)
+
+    def step(self):
+        self.forward()
+        self.commit()

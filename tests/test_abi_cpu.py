@@ -2,13 +2,14 @@
 rejects bad arguments on the host before touching a device.  No kernel runs
 here (none of these calls gets past argument validation)."""
 import ctypes
+import glob
 import os
 import re
 
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "wedlm.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 LIB = os.path.join(ROOT, "paper_2512_22737_amd", "libwedlm.so")
 
 pytestmark = pytest.mark.skipif(not os.path.exists(LIB),
@@ -16,7 +17,7 @@ pytestmark = pytest.mark.skipif(not os.path.exists(LIB),
 
 
 def declared_symbols():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(wedlm_\w+)\s*\(", text)))
 
@@ -137,3 +138,79 @@ def test_commit_rejects_bad_arguments():
     bad = list(args)
     bad[21] = None
     assert lib.wedlm_commit(*bad) == -1            # status is required
+
+
+def test_reorder_gather_outputs_all_or_none():
+    lib = _lib()
+    f = _fake()
+    # indices only needs qkv_in and the three outputs all NULL; a mix fails
+    args = [f, f, None, 1, 16, 4, 2, 64, 1e6] + [f] * 4 + [f, None, None,
+                                                          None]
+    assert lib.wedlm_reorder(*args) == -1
+
+
+def _cfg(**kw):
+    from paper_2512_22737_amd import wedlm
+    d = dict(L=2, Hd=256, Hq=4, Hkv=2, D=64, I=512, V=1000, mask_token=999)
+    d.update(kw)
+    return wedlm.model_config(**d)
+
+
+def test_model_workspace_and_config_checks():
+    lib = _lib()
+    ws = lib.wedlm_model_workspace_size
+    good = _cfg()
+    n = ws(ctypes.byref(good), 2, 16, 300)
+    assert n > 0 and n % 256 == 0
+    # hidden not a multiple of 256, bad head dim, mask token outside V, W > 64
+    for bad in (_cfg(Hd=320), _cfg(D=96), _cfg(mask_token=1000),
+                _cfg(Hq=5)):
+        assert ws(ctypes.byref(bad), 2, 16, 300) == 0
+    assert ws(ctypes.byref(good), 2, 65, 300) == 0
+    assert ws(None, 2, 16, 300) == 0
+
+
+def test_linear_and_small_kernels_reject_bad_arguments():
+    lib = _lib()
+    f = _fake()
+    assert lib.wedlm_linear(f, f, 4, 48, 256, 0, f, 48, None) == -2  # N%32
+    assert lib.wedlm_linear(f, f, 4, 64, 200, 0, f, 64, None) == -2  # K%64
+    assert lib.wedlm_linear(f, f, 4, 64, 256, 3, f, 64, None) == -1  # epi
+    assert lib.wedlm_linear(f, f, 4, 64, 256, 0, f, 32, None) == -2  # ldo<N
+    assert lib.wedlm_linear(None, f, 4, 64, 256, 0, f, 64, None) == -1
+    assert lib.wedlm_rmsnorm(f, f, 4, 256, 0.0, f, None) == -1       # eps
+    assert lib.wedlm_rmsnorm(f, f, 4, 254, 1e-6, f, None) == -2
+    assert lib.wedlm_embed(f, 4, 1000, f, 1000, 256, f, None) == -2  # mask id
+    assert lib.wedlm_qk_norm_rope(f, f, f, f, 4, 4, 2, 96, 1e6, 1e-6, f, f,
+                                  f, None) == -2
+    assert lib.wedlm_qk_norm_rope(f, f, f, f, 4, 4, 2, 64, 1.0, 1e-6, f, f,
+                                  f, None) == -1
+
+
+def test_model_forward_and_commit_layers_reject_bad_arguments():
+    from paper_2512_22737_amd import wedlm
+    lib = _lib()
+    f = _fake()
+    cfg = _cfg()
+    w = wedlm.ModelWeights(*([0x1000] * len(wedlm.WEIGHT_NAMES)))
+    need = lib.wedlm_model_workspace_size(ctypes.byref(cfg), 2, 16, 300)
+    args = [ctypes.byref(cfg), ctypes.byref(w), f, f, 2, 16, f, f, 100, f, 20,
+            300, 0.1] + [f] * 4 + [f, f, f, f, None, f, f, need, None]
+    bad = list(args)
+    bad[-2] = need - 1
+    assert lib.wedlm_model_forward(*bad) == -3
+    bad = list(args)
+    bad[12] = 0.0
+    assert lib.wedlm_model_forward(*bad) == -1     # temperature
+    w0 = wedlm.ModelWeights(*([0x1000] * (len(wedlm.WEIGHT_NAMES) - 1) + [0]))
+    bad = list(args)
+    bad[1] = ctypes.byref(w0)
+    assert lib.wedlm_model_forward(*bad) == -1     # lm_head missing
+    cargs = [f, f, f, f, 0.9, 0.01, f, f, f, f, 100, f, 10, 2, 16, 2, 64, 2,
+             f, f, f, f, f, 0, None]
+    bad = list(cargs)
+    bad[17] = 0
+    assert lib.wedlm_commit_layers(*bad) == -2     # no layers
+    bad = list(cargs)
+    bad[23] = 7
+    assert lib.wedlm_commit_layers(*bad) == -1     # unknown rule
