@@ -20,6 +20,16 @@ several row counts and prints one JSON line per count with its roofline
 (intensity R flop per weight byte: HBM-bound below the ridge, MFMA-bound
 above it).
 
+--model instead runs the decoder around the step: a Qwen3-8B-shaped model
+(36 layers, hidden 4096, 32/8 heads of 128, MLP 12288, vocabulary 151936,
+random bf16 weights) on two batches, 1 sequence with a 2048-token prompt and
+16 sequences with 1024-token prompts, window W=32.  The prompt is prefilled
+through the window path itself (all-filled windows); then one streaming step
+(wedlm_model_forward + wedlm_commit_layers) is captured in a HIP graph and
+replayed.  One JSON line per batch: ms per step, window tokens/s, committed
+tokens/s, p_cache, and the step's HBM roofline (weights + the caches' keys
+and values read per step, over the step time, against 8 TB/s).
+
 --compare-rules instead runs the streaming workload (16 sequences, starting
 prefix 1024, W=32, V=151936, fresh synthetic logits every step) under each
 decoding rule of wedlm_commit_rule (Algorithm 1's streaming commit,
@@ -182,6 +192,107 @@ def bench_lm_head(args, dev):
             flush=True)
 
 
+def bench_model(args, dev):
+    import torch
+    from paper_2512_22737_amd import wedlm
+    from paper_2512_22737_amd import workloads as WL
+    ms = WL.MODEL_SHAPES["qwen3_8b"]
+    L = args.model_layers or ms.L
+    cfg = wedlm.model_config(L, ms.Hd, ms.Hq, ms.Hkv, ms.D, ms.I, ms.V,
+                             ms.mask_row, ms.theta, ms.eps)
+    print(f"# generating {L}-layer weights on the device", file=sys.stderr,
+          flush=True)
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed)
+    tens = {}
+    for name, shape in wedlm.weight_shapes(cfg).items():
+        t = torch.randn(shape, generator=g, device=dev, dtype=torch.bfloat16)
+        if name.endswith("norm"):
+            t.mul_(0.1).add_(1.0)
+        elif name != "embed":
+            t.mul_(1.0 / math.sqrt(shape[-1]))
+        if name in wedlm.PACKED:          # the projections' MFMA-tile layout
+            t = wedlm.pack(t)
+        tens[name] = t
+    w_bytes = sum(t.numel() * 2 for n, t in tens.items() if n != "embed")
+    W = 32
+    for B, c0 in ((1, 2048), (16, 1024)):
+        steps, warm = args.steps, args.warmup
+        per = -(-(c0 + (steps + warm + 2) * W) // 16)
+        bt = torch.arange(B * per, dtype=torch.int32,
+                          device=dev).view(B, per)
+        dec = wedlm.Decoder(cfg, tens, B, W, B * per, bt,
+                            max_prefix_len=per * 16, temperature=0.1,
+                            packed=True)
+        gp = torch.Generator(device=dev)
+        gp.manual_seed(args.seed + 1)
+        prompt = torch.randint(0, ms.V - 1, (B, c0), generator=gp,
+                               device=dev, dtype=torch.int32)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(c0 // W):
+            dec.win_tok.copy_(prompt[:, k * W:(k + 1) * W])
+            dec.step()
+        torch.cuda.synchronize()
+        prefill_s = time.perf_counter() - t0
+        # eager steps (host launch cost included), then the graph
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        for _ in range(2):
+            dec.step()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(3):
+            dec.step()
+        e1.record()
+        torch.cuda.synchronize()
+        eager_ms = e0.elapsed_time(e1) / 3
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            dec.step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            dec.step()
+        for _ in range(warm):
+            graph.replay()
+        torch.cuda.synchronize()
+        c_before = dec.win_start.clone()
+        kv_pos = int(c_before.sum())
+        e0.record()
+        for _ in range(steps):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms_step = e0.elapsed_time(e1) / steps
+        committed = int((dec.win_start - c_before).sum())
+        st = int((dec.status != 0).sum() + (dec.attn_status != 0).sum())
+        # bytes a step must move: every weight but the embedding (a few rows
+        # of it) and the keys and values of each sequence's prefix in every
+        # layer, at the prefix length halfway through the timed steps
+        kv_per_pos = 2 * ms.Hkv * ms.D * 2 * L
+        kv_bytes = kv_per_pos * (kv_pos + committed / 2)
+        alg = w_bytes + kv_bytes
+        gbps = alg / (ms_step * 1e-3) / 1e9
+        print(json.dumps({
+            "kind": "model_step", "model": "qwen3_8b_shaped", "layers": L,
+            "B": B, "W": W, "prompt": c0, "steps": steps, "warmup": warm,
+            "ms_per_step": ms_step, "eager_ms_per_step": eager_ms,
+            "window_tokens_per_s": B * W / (ms_step * 1e-3),
+            "committed_tokens_per_s": committed / (steps * ms_step * 1e-3),
+            "p_cache": committed / (steps * B * W),
+            "prefill_tokens_per_s": B * c0 / prefill_s,
+            "weight_bytes": w_bytes, "kv_bytes_per_step": kv_bytes,
+            "roofline": {"bound": "hbm", "achieved": gbps,
+                         "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": gbps / HBM_PEAK_GBPS},
+            "status_nonzero": st, "data": "synthetic"}), flush=True)
+        del dec
+        torch.cuda.synchronize()
+
+
 def compare_rules(args, dev):
     """Decoding rules on the streaming workload: every run starts from the
     same all-mask windows at prefix 1024 and draws the same per-step logits
@@ -272,6 +383,10 @@ def main():
     ap.add_argument("--rule-steps", type=int, default=128)
     ap.add_argument("--lm-head", action="store_true",
                     help="time the fused output layer + score, then exit")
+    ap.add_argument("--model", action="store_true",
+                    help="time the Qwen3-8B-shaped decoder step, then exit")
+    ap.add_argument("--model-layers", type=int, default=0,
+                    help="layers of --model (default: 36)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for "
                          "scaling HBM counters) and exit")
@@ -306,6 +421,9 @@ def main():
         return
     if args.lm_head:
         bench_lm_head(args, dev)
+        return
+    if args.model:
+        bench_model(args, dev)
         return
 
     wl = WL.WORKLOADS[args.workload]

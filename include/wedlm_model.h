@@ -49,8 +49,10 @@ typedef struct {
   float rms_eps;      /* RMSNorm epsilon (> 0)                            */
 } wedlm_model_config;
 
-/* Weights, bf16, stacked over layers.  Every projection is [out, in]: one
- * row per output feature. */
+/* Weights, bf16, stacked over layers.  Every projection is [out, in] (one
+ * row per output feature) in the PACKED layout of wedlm_pack_weights, each
+ * layer's matrix packed on its own; embeddings, norms and the output layer
+ * are plain row-major. */
 typedef struct {
   const uint16_t* embed;      /* [V, Hd]                                  */
   const uint16_t* attn_norm;  /* [L, Hd]                                  */
@@ -83,19 +85,43 @@ int wedlm_rmsnorm(const float* x, const uint16_t* gain, int32_t M,
                   int32_t Hd, float eps, uint16_t* y, void* stream);
 
 /*
+ * wedlm_pack_weights -- lay a row-major weight matrix w [rows, K] out in
+ * MFMA tiles, the layout wedlm_linear and the decoder read.  Tile (r, s)
+ * holds rows 32r .. 32r+31 and k = 64s .. 64s+63 and is 4 KB at element
+ * offset (r * K/64 + s) * 2048; inside it, the 8 values at element
+ * (j * 64 + l) * 8 are row 32r + l%32, k = 64s + 32*(l/32) + 8j .. +7
+ * (j = 0..3, l = 0..63): lane l's operand of the tile's j-th MFMA.
+ * rows a multiple of 32, K a multiple of 64; packed has rows * K elements
+ * and must not overlap w.  A one-time conversion of a checkpoint.
+ */
+int wedlm_pack_weights(const uint16_t* w, int64_t rows, int32_t K,
+                       uint16_t* packed, void* stream);
+
+/* Bytes of workspace wedlm_linear needs for this product (0: none, or an
+ * invalid shape). */
+size_t wedlm_linear_workspace_size(int32_t M, int32_t N, int32_t K,
+                                   int32_t epilogue);
+
+/*
  * wedlm_linear -- out = x W^T on bf16 MFMA with fp32 accumulation, summed
  * over K in a fixed order (the result does not depend on the run).
- *   x [M, K] bf16, w [rows, K] bf16, out [M, ldo] (ldo >= N);
+ *   x [M, K] bf16 row-major, w [rows, K] bf16 packed (wedlm_pack_weights),
+ *   out [M, ldo] (ldo >= N);
  *   epilogue WEDLM_EPI_STORE_BF16: rows = N, out bf16;
  *            WEDLM_EPI_ADD_F32:    rows = N, out fp32, added in place
  *                                  (the residual stream);
  *            WEDLM_EPI_SWIGLU:     rows = 2N (N gate rows, then N up rows),
  *                                  out bf16 = silu(gate) * up.
  *   N a multiple of 32, K a multiple of 64.  x and out must not overlap.
+ * workspace: wedlm_linear_workspace_size() bytes (NULL when that is 0):
+ * the fp32 partial products of a residual-add product whose K is split over
+ * workgroups, summed into out in split order by a second kernel; its
+ * contents on entry do not matter.  Two calls that overlap in time must not
+ * share a workspace.
  */
 int wedlm_linear(const uint16_t* x, const uint16_t* w, int32_t M, int32_t N,
                  int32_t K, int32_t epilogue, void* out, int32_t ldo,
-                 void* stream);
+                 void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * wedlm_qk_norm_rope -- split one row of q|k|v (the output of W_qkv), RMSNorm

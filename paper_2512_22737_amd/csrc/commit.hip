@@ -63,6 +63,117 @@ __device__ __noinline__ double adjusted_of(double h, double lam, int d) {
 }
 #pragma clang fp contract(on)
 
+// The committed run of sequence b, computed by wave 0 (lane s = window slot
+// s): its length n under the rule, the prefix length c, the cache slot of
+// each committed position, and the status bits when a committed position
+// has no page inside the cache (then nothing is committed).
+struct Run {
+  int t;                  // the lane's window token
+  bool in, is_mask;
+  uint64_t maskb;         // ballot of the mask slots
+  int n_o, s0, n, c, slot, bad;
+};
+
+__device__ Run committed_run(const CommitArgs& a, int b) {
+  Run r;
+  const int W = a.W;
+  const int s = threadIdx.x;
+  r.in = s < W;
+  r.t = r.in ? a.win_tok[b * W + s] : 0;
+  r.is_mask = r.in && r.t < 0;
+  r.maskb = ballot(r.is_mask);
+  const uint64_t filledb = ballot(r.in && !r.is_mask);
+  r.n_o = __popcll(filledb);
+  r.s0 = r.maskb ? __ffsll(static_cast<long long>(r.maskb)) - 1 : W;
+  r.n = (a.rule == WEDLM_RULE_BLOCK) ? (r.maskb ? 0 : W) : r.s0;
+  r.c = a.win_start[b];
+  const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
+  // every committed position must have a page inside the cache
+  int why = 0;
+  r.slot = -1;
+  if (s < r.n) {
+    const int64_t p = static_cast<int64_t>(r.c) + s;
+    const int64_t blk = p / kPage;
+    if (r.c < 0 || blk >= a.max_pages) {
+      why = WEDLM_SEQ_CAPACITY;
+    } else {
+      const int id = bt[blk];
+      if (id < 0 || id >= a.num_pages) why = WEDLM_SEQ_BAD_PAGE;
+      else r.slot = id * kPage + static_cast<int>(p % kPage);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) why |= __shfl_xor(why, off);
+  r.bad = why;
+  return r;
+}
+
+// KV extend: physical rows 0..n-1 -> positions c..c+n-1 of the caches of
+// layers [l0, l1), 16-byte pieces of D/8 bf16 values, spread over the
+// workgroup's threads.  K rows are contiguous in both layouts.  For V the
+// lanes run over consecutive rows of one (head, 8 values of d), so the
+// transposed stores of one page land in contiguous 32-byte rows.
+__device__ void append_rows(const CommitArgs& a, int b, int n, int c, int l0,
+                            int l1) {
+  const int W = a.W, D = a.D, Hkv = a.Hkv;
+  const int DG = D / 8;
+  const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
+  const int total = n * Hkv * DG;
+  for (int e2 = threadIdx.x; e2 < total * (l1 - l0); e2 += kThreads) {
+    const int l = l0 + e2 / total, e = e2 % total;
+    const uint16_t* k_phys = a.k_phys + l * a.win_lstride;
+    const uint16_t* v_phys = a.v_phys + l * a.win_lstride;
+    uint16_t* k_cache = a.k_cache + l * a.cache_lstride;
+    uint16_t* v_cache = a.v_cache + l * a.cache_lstride;
+    // K: e = (j, h, dg), dg fastest
+    {
+      const int dg = e % DG;
+      const int jh = e / DG;
+      const int h = jh % Hkv;
+      const int j = jh / Hkv;
+      const int p = c + j;
+      const int64_t pg = bt[p / kPage];
+      const int row = p % kPage;
+      const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
+          k_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
+      *reinterpret_cast<u16x8_t*>(
+          k_cache + ((pg * Hkv + h) * kPage + row) * D + dg * 8) = v;
+    }
+    // V: e = (h, dg, j), j fastest
+    {
+      const int j = e % n;
+      const int hd = e / n;
+      const int dg = hd % DG;
+      const int h = hd / DG;
+      const int p = c + j;
+      const int64_t pg = bt[p / kPage];
+      const int row = p % kPage;
+      const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
+          v_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
+      uint16_t* dst = v_cache + ((pg * Hkv + h) * D + dg * 8) * kPage + row;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) dst[k * kPage] = v[k];
+    }
+  }
+}
+
+// Extends the caches of layer blockIdx.y of sequence blockIdx.x before
+// commit_kernel updates the window (it reads the same pre-step state and
+// finds the same run).
+__global__ __launch_bounds__(kThreads) void kv_append_kernel(CommitArgs a) {
+  const int b = blockIdx.x, l = blockIdx.y;
+  __shared__ int s_n, s_c;
+  if (threadIdx.x < kWave) {
+    const Run r = committed_run(a, b);
+    if (threadIdx.x == 0) {
+      s_n = r.bad ? 0 : r.n;
+      s_c = r.c;
+    }
+  }
+  __syncthreads();
+  if (s_n > 0) append_rows(a, b, s_n, s_c, l, l + 1);
+}
+
 __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
   const int b = blockIdx.x;
   const int W = a.W;
@@ -70,33 +181,11 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
 
   if (threadIdx.x < kWave) {
     const int s = threadIdx.x;
-    const bool in = s < W;
-    int t = in ? a.win_tok[b * W + s] : 0;
-    const bool is_mask = in && t < 0;
-    const uint64_t maskb = ballot(is_mask);
-    const uint64_t filledb = ballot(in && !is_mask);
-    const int n_o = __popcll(filledb);
-    const int s0 = maskb ? __ffsll(static_cast<long long>(maskb)) - 1 : W;
-    const int n = (a.rule == WEDLM_RULE_BLOCK) ? (maskb ? 0 : W) : s0;
-    const int c = a.win_start[b];
-    const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
-
-    // every committed position must have a page inside the cache
-    int slot = -1, why = 0;
-    if (s < n) {
-      const int64_t p = static_cast<int64_t>(c) + s;
-      const int64_t blk = p / kPage;
-      if (c < 0 || blk >= a.max_pages) {
-        why = WEDLM_SEQ_CAPACITY;
-      } else {
-        const int id = bt[blk];
-        if (id < 0 || id >= a.num_pages) why = WEDLM_SEQ_BAD_PAGE;
-        else slot = id * kPage + static_cast<int>(p % kPage);
-      }
-    }
-    int bad = why;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) bad |= __shfl_xor(bad, off);
+    const Run r = committed_run(a, b);
+    const bool in = r.in, is_mask = r.is_mask;
+    const int t = r.t, n_o = r.n_o, s0 = r.s0, n = r.n, c = r.c;
+    const uint64_t maskb = r.maskb;
+    const int slot = r.slot, bad = r.bad;
 
     if (bad) {
       if (in) {
@@ -159,51 +248,7 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
   __syncthreads();
   if (!s_ok) return;
 
-  // KV extend: physical rows 0..n-1 -> positions c..c+n-1, 16-byte pieces
-  // of D/8 bf16 values.  K rows are contiguous in both layouts.  For V the
-  // lanes run over consecutive rows of one (head, 8 values of d), so the
-  // transposed stores of one page land in contiguous 32-byte rows.
-  const int n = s_n, c = s_c;
-  const int D = a.D, Hkv = a.Hkv;
-  const int DG = D / 8;
-  const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
-  const int total = n * Hkv * DG;
-  for (int e2 = threadIdx.x; e2 < total * a.n_layers; e2 += kThreads) {
-    const int l = e2 / total, e = e2 - l * total;
-    const uint16_t* k_phys = a.k_phys + l * a.win_lstride;
-    const uint16_t* v_phys = a.v_phys + l * a.win_lstride;
-    uint16_t* k_cache = a.k_cache + l * a.cache_lstride;
-    uint16_t* v_cache = a.v_cache + l * a.cache_lstride;
-    // K: e = (j, h, dg), dg fastest
-    {
-      const int dg = e % DG;
-      const int jh = e / DG;
-      const int h = jh % Hkv;
-      const int j = jh / Hkv;
-      const int p = c + j;
-      const int64_t pg = bt[p / kPage];
-      const int row = p % kPage;
-      const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
-          k_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
-      *reinterpret_cast<u16x8_t*>(
-          k_cache + ((pg * Hkv + h) * kPage + row) * D + dg * 8) = v;
-    }
-    // V: e = (h, dg, j), j fastest
-    {
-      const int j = e % n;
-      const int hd = e / n;
-      const int dg = hd % DG;
-      const int h = hd / DG;
-      const int p = c + j;
-      const int64_t pg = bt[p / kPage];
-      const int row = p % kPage;
-      const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
-          v_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
-      uint16_t* dst = v_cache + ((pg * Hkv + h) * D + dg * 8) * kPage + row;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) dst[k * kPage] = v[k];
-    }
-  }
+  if (s_n > 0) append_rows(a, b, s_n, s_c, 0, a.n_layers);
 }
 
 }  // namespace
@@ -245,8 +290,17 @@ int commit_impl(int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
   a.n_layers = n_layers;
   a.win_lstride = static_cast<int64_t>(B) * W * Hkv * D;
   a.cache_lstride = num_pages * Hkv * kPage * D;
-  hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(kThreads), 0,
-                     static_cast<hipStream_t>(stream), a);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n_layers > 1) {
+    // one workgroup per (sequence, layer), before the window changes; the
+    // commit kernel then extends no cache
+    if (n_layers > 65535) return WEDLM_E_SHAPE;
+    hipLaunchKernelGGL(kv_append_kernel, dim3(B, n_layers), dim3(kThreads), 0,
+                       st, a);
+    WEDLM_LAUNCH_CHECK();
+    a.n_layers = 0;
+  }
+  hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(kThreads), 0, st, a);
   WEDLM_LAUNCH_CHECK();
   return WEDLM_OK;
 }

@@ -17,10 +17,18 @@
 //   MFMA      = v_mfma_f32_32x32x16_bf16, A = weight rows (features), B =
 //               activation rows (tokens); lane l holds row l%32 and, in each
 //               64-wide k step, lane half hf of MFMA j takes k = 32hf + 8j
-//               .. +8 of both operands: 64 contiguous bytes per lane per step
-//               (four 16-byte loads that share two 128-byte lines).
+//               .. +8 of both operands.
+//   weights   = packed in MFMA tiles (wedlm_pack_weights): the 32 rows x 64
+//               k of one block and step are 4 KB in the order the MFMAs read
+//               them, lane l's 16 bytes of MFMA j at byte 1024j + 16l, so
+//               each load instruction reads 1 KB of contiguous memory and a
+//               wave's run of steps is one contiguous stretch.  Activations
+//               stay row-major: lane l reads 64 contiguous bytes of its token
+//               row per step (from L2).
 //   output    = lane l, element e: feature 8(e/4) + 4(l/32) + e%4, token l%32.
 #include <math.h>
+
+#include <algorithm>
 
 #include "common.h"
 #include "wedlm_model.h"
@@ -56,30 +64,45 @@ __global__ __launch_bounds__(256) void embed_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// RMSNorm: y = bf16(x / sqrt(mean(x^2) + eps) * g), one workgroup per row
+// RMSNorm: y = bf16(x / sqrt(mean(x^2) + eps) * g), one workgroup per row.
+// With ADD, the n_ks partial products of a split residual-add projection
+// ([n_ks, M, Hd] fp32) are first added into x in split order and the sum is
+// written back (the residual stream), then normalised.
 // ---------------------------------------------------------------------------
 constexpr int kNormThreads = 256;
 
+template <bool ADD>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
-    const float* __restrict__ x, const uint16_t* __restrict__ g, int Hd,
-    float eps, uint16_t* __restrict__ y) {
+    float* __restrict__ x, const float* __restrict__ part, int n_ks, int M,
+    const uint16_t* __restrict__ g, int Hd, float eps,
+    uint16_t* __restrict__ y) {
   const int t = blockIdx.x;
-  const float* row = x + static_cast<int64_t>(t) * Hd;
+  float* row = x + static_cast<int64_t>(t) * Hd;
   float ss = 0.f;
   for (int c = threadIdx.x; c < Hd / 4; c += kNormThreads) {
-    const floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
+    floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
+    if constexpr (ADD) {
+      for (int k = 0; k < n_ks; ++k) {
+        const floatx4_t p = *reinterpret_cast<const floatx4_t*>(
+            part + (static_cast<int64_t>(k) * M + t) * Hd + c * 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] += p[e];
+      }
+      *reinterpret_cast<floatx4_t*>(row + c * 4) = v;
+    }
     ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-  __shared__ float part[kNormThreads / kWave];
-  if (lane_id() == 0) part[threadIdx.x / kWave] = ss;
+  __shared__ float wsum[kNormThreads / kWave];
+  if (lane_id() == 0) wsum[threadIdx.x / kWave] = ss;
   __syncthreads();
   float tot = 0.f;
 #pragma unroll
-  for (int i = 0; i < kNormThreads / kWave; ++i) tot += part[i];
+  for (int i = 0; i < kNormThreads / kWave; ++i) tot += wsum[i];
   const float r = 1.0f / sqrtf(tot / static_cast<float>(Hd) + eps);
   uint16_t* out = y + static_cast<int64_t>(t) * Hd;
+  // every thread re-reads only the chunks it wrote itself
   for (int c = threadIdx.x; c < Hd / 4; c += kNormThreads) {
     const floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
     const u16x4_t gg = *reinterpret_cast<const u16x4_t*>(g + c * 4);
@@ -178,16 +201,34 @@ constexpr int kRedStride = 33;                    // LDS row of 32 tokens + 1
 
 enum Epi { kStoreBf16 = 0, kAddF32 = 1, kSwiglu = 2 };
 
+constexpr int kTile = 32 * kKStep;               // elements of a packed tile
+
 struct GemmArgs {
   const uint16_t* x;      // [M, K] activations
-  const uint16_t* w;      // [rows, K] weights
+  const uint16_t* w;      // [rows, K] weights, packed tiles
   void* out;              // [M, ldo]
   int M, N, K, ldo;
-  int up_off;             // SwiGLU: first row of the up block
+  int up_blk;             // SwiGLU: first 32-row block of the up rows
   int n_nb, n_rg;         // 32-feature blocks, row groups
+  int n_ks;               // K splits over workgroups (residual add only)
+  float* part;            // n_ks > 1: [n_ks, M, N] partial products
 };
 
-template <int NB, int NA, int PF, int EPI>
+template <int EPI>
+__device__ __forceinline__ void gemm_store(const GemmArgs& a, int64_t o,
+                                           float g, float u) {
+  if constexpr (EPI == kStoreBf16) {
+    static_cast<uint16_t*>(a.out)[o] = f32_to_bf16(g);
+  } else if constexpr (EPI == kAddF32) {
+    static_cast<float*>(a.out)[o] += g;
+  } else {
+    static_cast<uint16_t*>(a.out)[o] = f32_to_bf16(g / (1.0f + expf(-g)) * u);
+  }
+}
+
+// NT: weight loads carry the non-temporal hint (one row group; with several,
+// the groups share the weight lines through L2)
+template <int NB, int NA, int PF, int EPI, bool NT>
 __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
   constexpr int RB = 32 * NB;
   constexpr int TPC = 2;                            // tiles per LDS round
@@ -195,9 +236,14 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
   static_assert(NB % BPC == 0 || NB < BPC, "row blocks per round");
   __shared__ float red[kGWaves * TPC * 32 * kRedStride];
 
+  // the K splits and row groups of one feature block sit on one XCD (same
+  // blockIdx % 8) at neighbouring positions: the row groups share its
+  // weight lines in that XCD's L2
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-  const int nb = xcd + 8 * (local / a.n_rg);
-  const int rg = local % a.n_rg;
+  const int per_nb = a.n_rg * a.n_ks;
+  const int nb = xcd + 8 * (local / per_nb);
+  const int rg = (local % per_nb) / a.n_ks;
+  const int ks = local % a.n_ks;
   if (nb >= a.n_nb) return;                         // whole workgroup
 
   const int lane = lane_id();
@@ -206,7 +252,9 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int col = lane & 31, hf = lane >> 5;
   const int S = a.K / kKStep;
-  const int s0 = wave * S / kGWaves, s1 = (wave + 1) * S / kGWaves;
+  const int k0 = ks * S / a.n_ks, k1 = (ks + 1) * S / a.n_ks;
+  const int s0 = k0 + wave * (k1 - k0) / kGWaves;
+  const int s1 = k0 + (wave + 1) * (k1 - k0) / kGWaves;
   const int n = s1 - s0;
 
   floatx16_t acc[NA][NB];
@@ -221,8 +269,8 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
     const uint16_t* wrow[NA];
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-      wrow[i] = a.w + static_cast<int64_t>(nb * 32 + col + i * a.up_off) * a.K +
-                hf * 32 + s0 * kKStep;
+      wrow[i] = a.w + (static_cast<int64_t>(nb + i * a.up_blk) * S + s0) * kTile +
+                lane * 8;
     const uint16_t* xrow[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -233,17 +281,24 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
     // every load is issued (steps past the run re-read its last step), so
     // the waits in the loop stay partial
     auto load = [&](int q, u16x8_t (&ra)[NA][4], u16x8_t (&rb)[NB][4]) {
-      const int off = min(q, n - 1) * kKStep;
+      const int qq = min(q, n - 1);
 #pragma unroll
       for (int i = 0; i < NA; ++i)
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          ra[i][u] = *reinterpret_cast<const u16x8_t*>(wrow[i] + off + u * 8);
+        for (int u = 0; u < 4; ++u) {
+          const u16x8_t* p = reinterpret_cast<const u16x8_t*>(
+              wrow[i] + qq * kTile + u * 512);
+          if constexpr (NT)
+            ra[i][u] = __builtin_nontemporal_load(p);
+          else
+            ra[i][u] = *p;
+        }
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-          rb[b][u] = *reinterpret_cast<const u16x8_t*>(xrow[b] + off + u * 8);
+          rb[b][u] = *reinterpret_cast<const u16x8_t*>(xrow[b] + qq * kKStep +
+                                                       u * 8);
     };
     auto mfma = [&](const u16x8_t (&ra)[NA][4], const u16x8_t (&rb)[NB][4]) {
 #pragma unroll
@@ -312,19 +367,49 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
           v[i] = s;
         }
         if (tok >= a.M) continue;
-        const int64_t o = static_cast<int64_t>(tok) * a.ldo + nb * 32 + f;
-        if constexpr (EPI == kStoreBf16) {
-          static_cast<uint16_t*>(a.out)[o] = f32_to_bf16(v[0]);
-        } else if constexpr (EPI == kAddF32) {
-          static_cast<float*>(a.out)[o] += v[0];
+        if (a.n_ks == 1) {
+          gemm_store<EPI>(a, static_cast<int64_t>(tok) * a.ldo + nb * 32 + f,
+                          v[0], v[NA - 1]);
         } else {
-          const float g = v[0], u = v[NA - 1];
-          static_cast<uint16_t*>(a.out)[o] =
-              f32_to_bf16(g / (1.0f + expf(-g)) * u);
+          // split K (residual add): this split's partial, summed into the
+          // residual stream later in split order
+          a.part[(static_cast<int64_t>(ks) * a.M + tok) * a.N + nb * 32 + f] =
+              v[0];
         }
       }
     }
   }
+}
+
+// x[t][n] += sum over splits k (in order) of part[k][t][n]
+__global__ __launch_bounds__(256) void add_partials_kernel(
+    float* __restrict__ x, int ldx, const float* __restrict__ part, int n_ks,
+    int M, int N) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= static_cast<int64_t>(M) * N) return;
+  const int t = static_cast<int>(i / N), n = static_cast<int>(i % N);
+  float v = x[static_cast<int64_t>(t) * ldx + n];
+  for (int k = 0; k < n_ks; ++k) v += part[static_cast<int64_t>(k) * M * N + i];
+  x[static_cast<int64_t>(t) * ldx + n] = v;
+}
+
+// row-major [rows, K] -> packed MFMA tiles; one thread moves 16 bytes and
+// the writes are contiguous
+__global__ __launch_bounds__(256) void pack_kernel(
+    const uint16_t* __restrict__ w, int K, int64_t n_chunks,
+    uint16_t* __restrict__ packed) {
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (c >= n_chunks) return;
+  const int S = K / kKStep;
+  const int64_t tile = c >> 8;                     // 256 chunks per tile
+  const int idx = static_cast<int>(c & 255);
+  const int u = idx >> 6, l = idx & 63;
+  const int64_t rb = tile / S;
+  const int s = static_cast<int>(tile - rb * S);
+  const int64_t row = rb * 32 + (l & 31);
+  const int k = s * kKStep + (l >> 5) * 32 + u * 8;
+  *reinterpret_cast<u16x8_t*>(packed + c * 8) =
+      *reinterpret_cast<const u16x8_t*>(w + row * K + k);
 }
 
 // rows per group: 32, 64, then 128 (64 for SwiGLU, two weight blocks)
@@ -334,10 +419,19 @@ int gemm_nb(int M, bool swiglu) {
   return 4;
 }
 
+// the largest row block of each kernel family also serves several row
+// groups; the smaller ones only ever run as one
 template <int NB, int NA, int PF, int EPI>
 void gemm_launch(const GemmArgs& a, hipStream_t st) {
-  const int64_t grid = 8ll * a.n_rg * ((a.n_nb + 7) / 8);
-  hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI>), dim3(grid),
+  const int64_t grid = 8ll * a.n_rg * a.n_ks * ((a.n_nb + 7) / 8);
+  if constexpr (NB * NA == 4) {
+    if (a.n_rg > 1) {
+      hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, false>), dim3(grid),
+                         dim3(kGThreads), 0, st, a);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, true>), dim3(grid),
                      dim3(kGThreads), 0, st, a);
 }
 
@@ -347,18 +441,57 @@ bool gemm_shape_ok(int M, int N, int K) {
          static_cast<int64_t>(N) * K * 2 < (1ll << 40);
 }
 
+size_t up256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+// The plan of one product: row block, row groups and K splits.  A residual-
+// add product (N = hidden: few feature blocks) splits K over workgroups
+// until about one workgroup per CU streams weights, never below one step
+// per wave; the splits write fp32 partials ([n_ks, M, N]) that the next
+// RMSNorm (or, standing alone, add_partials_kernel) sums into the residual
+// stream in split order.  No workgroup waits for another.
+struct GemmPlan {
+  int nb, n_nb, n_rg, n_ks;
+  size_t part_bytes;
+};
+
+constexpr int kGemmTargetWgs = 256;
+
+GemmPlan gemm_plan(int M, int N, int K, int epi) {
+  GemmPlan p{};
+  p.nb = gemm_nb(M, epi == kSwiglu);
+  p.n_nb = N / 32;
+  p.n_rg = (M + 32 * p.nb - 1) / (32 * p.nb);
+  p.n_ks = 1;
+  if (epi == kAddF32) {
+    const int wgs = p.n_nb * p.n_rg;
+    p.n_ks = std::max(1, std::min(kGemmTargetWgs / wgs, K / kKStep / kGWaves));
+  }
+  if (p.n_ks > 1)
+    p.part_bytes = static_cast<size_t>(p.n_ks) * M * N * sizeof(float);
+  return p;
+}
+
+// Launches the product; with K split, the partials go to `part` and the
+// caller adds them (defer) or add_partials_kernel does right after.
 int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
-         int ldo, int epi, hipStream_t st) {
+         int ldo, int epi, void* part, size_t part_bytes, bool defer,
+         hipStream_t st, int* n_ks_out = nullptr) {
   if (!x || !w || !out) return WEDLM_E_ARG;
   if (epi != kStoreBf16 && epi != kAddF32 && epi != kSwiglu) return WEDLM_E_ARG;
   if (!gemm_shape_ok(M, N, K) || ldo < N) return WEDLM_E_SHAPE;
+  const GemmPlan p = gemm_plan(M, N, K, epi);
+  if (p.part_bytes > 0 && (!part || part_bytes < p.part_bytes))
+    return WEDLM_E_WORKSPACE;
   GemmArgs a{};
   a.x = x; a.w = w; a.out = out; a.M = M; a.N = N; a.K = K; a.ldo = ldo;
-  a.up_off = N;
-  const int nb = gemm_nb(M, epi == kSwiglu);
-  a.n_nb = N / 32;
-  a.n_rg = (M + 32 * nb - 1) / (32 * nb);
-  if (8ll * a.n_rg * ((a.n_nb + 7) / 8) > (1ll << 30)) return WEDLM_E_SHAPE;
+  a.up_blk = N / 32;
+  a.n_nb = p.n_nb;
+  a.n_rg = p.n_rg;
+  a.n_ks = p.n_ks;
+  a.part = static_cast<float*>(part);
+  if (8ll * a.n_rg * a.n_ks * ((a.n_nb + 7) / 8) > (1ll << 30))
+    return WEDLM_E_SHAPE;
+  const int nb = p.nb;
   if (epi == kSwiglu) {
     if (nb == 1) gemm_launch<1, 2, 2, kSwiglu>(a, st);
     else gemm_launch<2, 2, 2, kSwiglu>(a, st);
@@ -371,6 +504,27 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
     else if (nb == 2) gemm_launch<2, 1, 2, kStoreBf16>(a, st);
     else gemm_launch<4, 1, 2, kStoreBf16>(a, st);
   }
+  WEDLM_LAUNCH_CHECK();
+  if (n_ks_out) *n_ks_out = p.n_ks;
+  if (p.n_ks > 1 && !defer) {
+    const int64_t total = static_cast<int64_t>(M) * N;
+    hipLaunchKernelGGL(add_partials_kernel, dim3((total + 255) / 256),
+                       dim3(256), 0, st, static_cast<float*>(out), ldo,
+                       a.part, p.n_ks, M, N);
+    WEDLM_LAUNCH_CHECK();
+  }
+  return WEDLM_OK;
+}
+
+// RMSNorm of the residual stream, first adding pending split partials
+int norm(float* x, const float* part, int n_ks, int M, int Hd,
+         const uint16_t* g, float eps, uint16_t* y, hipStream_t st) {
+  if (part && n_ks > 1)
+    hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(M), dim3(kNormThreads), 0,
+                       st, x, part, n_ks, M, g, Hd, eps, y);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(M), dim3(kNormThreads), 0,
+                       st, x, nullptr, 0, M, g, Hd, eps, y);
   WEDLM_LAUNCH_CHECK();
   return WEDLM_OK;
 }
@@ -386,10 +540,10 @@ bool config_ok(const wedlm_model_config* c) {
 
 // workspace carve-up of the forward, 256-byte aligned pieces
 struct Carve {
-  size_t x, xn, qkv, q, attn, act, attn_ws, lm_ws, total;
+  size_t part, x, xn, qkv, q, attn, act, attn_ws, lm_ws, total;
+  size_t part_bytes;
 };
 
-size_t up256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
 Carve carve(const wedlm_model_config* c, int B, int W, int max_prefix_len) {
   const size_t M = static_cast<size_t>(B) * W;
@@ -397,6 +551,13 @@ Carve carve(const wedlm_model_config* c, int B, int W, int max_prefix_len) {
   const size_t Hq = c->n_heads, Hkv = c->n_kv_heads;
   Carve k{};
   size_t off = 0;
+  // split partials of the two residual-add products (each is summed by the
+  // next RMSNorm before the other is written)
+  const int Mi = static_cast<int>(M);
+  k.part_bytes = std::max(
+      gemm_plan(Mi, c->hidden, c->n_heads * c->head_dim, kAddF32).part_bytes,
+      gemm_plan(Mi, c->hidden, c->inter, kAddF32).part_bytes);
+  k.part = off; off += up256(k.part_bytes);
   k.x = off;    off += up256(M * Hd * 4);
   k.xn = off;   off += up256(M * Hd * 2);
   k.qkv = off;  off += up256(M * (Hq + 2 * Hkv) * D * 2);
@@ -439,17 +600,40 @@ extern "C" int wedlm_rmsnorm(const float* x, const uint16_t* gain, int32_t M,
                              void* stream) {
   if (!x || !gain || !y || !(eps > 0.f)) return WEDLM_E_ARG;
   if (M < 1 || Hd < 4 || Hd % 4 != 0) return WEDLM_E_SHAPE;
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(kNormThreads), 0,
-                     static_cast<hipStream_t>(stream), x, gain, Hd, eps, y);
+  // without partials the kernel only reads x
+  return norm(const_cast<float*>(x), nullptr, 0, M, Hd, gain, eps, y,
+              static_cast<hipStream_t>(stream));
+}
+
+extern "C" int wedlm_pack_weights(const uint16_t* w, int64_t rows, int32_t K,
+                                  uint16_t* packed, void* stream) {
+  if (!w || !packed) return WEDLM_E_ARG;
+  if (rows < 32 || rows % 32 != 0 || K < kKStep || K % kKStep != 0)
+    return WEDLM_E_SHAPE;
+  const int64_t n_chunks = rows * K / 8;
+  const int64_t grid = (n_chunks + 255) / 256;
+  if (grid > 0x7fffffffll) return WEDLM_E_SHAPE;
+  hipLaunchKernelGGL(pack_kernel, dim3(static_cast<unsigned>(grid)), dim3(256),
+                     0, static_cast<hipStream_t>(stream), w, K, n_chunks,
+                     packed);
   WEDLM_LAUNCH_CHECK();
   return WEDLM_OK;
 }
 
+extern "C" size_t wedlm_linear_workspace_size(int32_t M, int32_t N,
+                                              int32_t K, int32_t epilogue) {
+  if (!gemm_shape_ok(M, N, K) ||
+      (epilogue != kStoreBf16 && epilogue != kAddF32 && epilogue != kSwiglu))
+    return 0;
+  return gemm_plan(M, N, K, epilogue).part_bytes;
+}
+
 extern "C" int wedlm_linear(const uint16_t* x, const uint16_t* w, int32_t M,
                             int32_t N, int32_t K, int32_t epilogue, void* out,
-                            int32_t ldo, void* stream) {
-  return gemm(x, w, M, N, K, out, ldo, epilogue,
-              static_cast<hipStream_t>(stream));
+                            int32_t ldo, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  return gemm(x, w, M, N, K, out, ldo, epilogue, workspace, workspace_bytes,
+              false, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int wedlm_qk_norm_rope(const uint16_t* qkv, const uint16_t* q_gain,
@@ -511,6 +695,8 @@ extern "C" int wedlm_model_forward(
   uint16_t* q = reinterpret_cast<uint16_t*>(ws + cv.q);
   uint16_t* attn = reinterpret_cast<uint16_t*>(ws + cv.attn);
   uint16_t* act = reinterpret_cast<uint16_t*>(ws + cv.act);
+  float* part = reinterpret_cast<float*>(ws + cv.part);
+  const size_t part_bytes = cv.part_bytes;
   void* attn_ws = ws + cv.attn_ws;
   void* lm_ws = ws + cv.lm_ws;
   const size_t attn_ws_bytes = cv.lm_ws - cv.attn_ws;
@@ -533,13 +719,17 @@ extern "C" int wedlm_model_forward(
                           nullptr, nullptr, nullptr, stream));
   WEDLM_TRY(wedlm_embed(tok_phys, M, cfg->mask_token, wt->embed, cfg->vocab,
                         Hd, x, stream));
+  // pend > 1: split partials of the last residual-add product, summed into
+  // x by the next RMSNorm
+  int pend = 0;
   for (int l = 0; l < cfg->n_layers; ++l) {
     uint16_t* kl = k_win + l * win_stride;
     uint16_t* vl = v_win + l * win_stride;
-    WEDLM_TRY(wedlm_rmsnorm(x, wt->attn_norm + static_cast<int64_t>(l) * Hd,
-                            M, Hd, cfg->rms_eps, xn, stream));
+    WEDLM_TRY(norm(x, part, pend, M, Hd,
+                   wt->attn_norm + static_cast<int64_t>(l) * Hd, cfg->rms_eps,
+                   xn, st));
     WEDLM_TRY(gemm(xn, wt->w_qkv + static_cast<int64_t>(l) * QKV * Hd, M, QKV,
-                   Hd, qkv, QKV, kStoreBf16, st));
+                   Hd, qkv, QKV, kStoreBf16, nullptr, 0, true, st));
     WEDLM_TRY(wedlm_qk_norm_rope(qkv, wt->q_norm + static_cast<int64_t>(l) * D,
                                  wt->k_norm + static_cast<int64_t>(l) * D,
                                  pos_ids, M, Hq, Hkv, D, cfg->rope_theta,
@@ -550,15 +740,17 @@ extern "C" int wedlm_model_forward(
         max_prefix_len, scale, attn, nullptr, status, attn_ws, attn_ws_bytes,
         stream));
     WEDLM_TRY(gemm(attn, wt->w_o + static_cast<int64_t>(l) * Hd * Hq * D, M,
-                   Hd, Hq * D, x, Hd, kAddF32, st));
-    WEDLM_TRY(wedlm_rmsnorm(x, wt->mlp_norm + static_cast<int64_t>(l) * Hd, M,
-                            Hd, cfg->rms_eps, xn, stream));
+                   Hd, Hq * D, x, Hd, kAddF32, part, part_bytes, true, st,
+                   &pend));
+    WEDLM_TRY(norm(x, part, pend, M, Hd,
+                   wt->mlp_norm + static_cast<int64_t>(l) * Hd, cfg->rms_eps,
+                   xn, st));
     WEDLM_TRY(gemm(xn, wt->w_gate_up + static_cast<int64_t>(l) * 2 * I * Hd, M,
-                   I, Hd, act, I, kSwiglu, st));
+                   I, Hd, act, I, kSwiglu, nullptr, 0, true, st));
     WEDLM_TRY(gemm(act, wt->w_down + static_cast<int64_t>(l) * Hd * I, M, Hd,
-                   I, x, Hd, kAddF32, st));
+                   I, x, Hd, kAddF32, part, part_bytes, true, st, &pend));
   }
-  WEDLM_TRY(wedlm_rmsnorm(x, wt->final_norm, M, Hd, cfg->rms_eps, xn, stream));
+  WEDLM_TRY(norm(x, part, pend, M, Hd, wt->final_norm, cfg->rms_eps, xn, st));
   WEDLM_TRY(wedlm_lm_head_score(xn, wt->lm_head, M, Hd, cfg->vocab,
                                 temperature, argmax, entropy, pmax, lm_ws,
                                 lm_ws_bytes, stream));

@@ -73,7 +73,11 @@ def _load():
     lib.wedlm_embed.restype = ctypes.c_int
     lib.wedlm_rmsnorm.argtypes = [P, P, I32, I32, F, P, P]
     lib.wedlm_rmsnorm.restype = ctypes.c_int
-    lib.wedlm_linear.argtypes = [P, P, I32, I32, I32, I32, P, I32, P]
+    lib.wedlm_pack_weights.argtypes = [P, I64, I32, P, P]
+    lib.wedlm_pack_weights.restype = ctypes.c_int
+    lib.wedlm_linear_workspace_size.argtypes = [I32, I32, I32, I32]
+    lib.wedlm_linear_workspace_size.restype = SZ
+    lib.wedlm_linear.argtypes = [P, P, I32, I32, I32, I32, P, I32, P, SZ, P]
     lib.wedlm_linear.restype = ctypes.c_int
     lib.wedlm_qk_norm_rope.argtypes = [P, P, P, P, I32, I32, I32, I32, D_, F,
                                        P, P, P, P]
@@ -105,7 +109,9 @@ EXPORTED = ["wedlm_reorder", "wedlm_window_attn_workspace_size",
             "wedlm_commit", "wedlm_commit_rule",
             "wedlm_lm_head_score_workspace_size", "wedlm_lm_head_score",
             "wedlm_strerror", "wedlm_version", "wedlm_embed", "wedlm_rmsnorm",
-            "wedlm_linear", "wedlm_qk_norm_rope", "wedlm_model_workspace_size",
+            "wedlm_linear", "wedlm_linear_workspace_size",
+            "wedlm_pack_weights", "wedlm_qk_norm_rope",
+            "wedlm_model_workspace_size",
             "wedlm_model_forward", "wedlm_commit_layers"]
 
 # decoding rules of wedlm_commit_rule (include/wedlm.h)
@@ -461,18 +467,53 @@ def wedlm_rmsnorm(x, gain, eps: float, y) -> None:
     _check(code, "wedlm_rmsnorm")
 
 
-def wedlm_linear(x, w, epilogue: int, out) -> None:
+def wedlm_pack_weights(w, packed) -> None:
+    """Row-major w [rows, K] -> the packed MFMA-tile layout (same shape)."""
+    rows, K = w.shape
+    code = _load().wedlm_pack_weights(
+        _t(w, "w", _BF16), rows, K, _t(packed, "packed", _BF16, (rows, K)),
+        _stream())
+    _check(code, "wedlm_pack_weights")
+
+
+def pack(w):
+    """A packed copy of a row-major weight matrix (or a stack of them, each
+    matrix packed on its own)."""
+    out = torch.empty_like(w)
+    if w.dim() == 2:
+        wedlm_pack_weights(w, out)
+    else:
+        for i in range(w.shape[0]):
+            wedlm_pack_weights(w[i], out[i])
+    return out
+
+
+PACKED = ("w_qkv", "w_o", "w_gate_up", "w_down")
+
+
+def wedlm_linear_workspace_size(M, N, K, epilogue) -> int:
+    return int(_load().wedlm_linear_workspace_size(M, N, K, epilogue))
+
+
+def wedlm_linear(x, w, epilogue: int, out, workspace=None) -> None:
     """out = x w^T with the epilogue of include/wedlm_model.h; x [M, K],
-    w [rows, K] (rows = 2N for SwiGLU), out [M, ldo] with ldo >= N."""
+    w [rows, K] packed (pack()), rows = 2N for SwiGLU; out [M, ldo] with
+    ldo >= N.  A workspace is allocated here if one is needed and none is
+    given."""
     M, K = x.shape
     rows = w.shape[0]
     N = rows // 2 if epilogue == EPI_SWIGLU else rows
     odt = (torch.float32,) if epilogue == EPI_ADD_F32 else _BF16
     if out.dim() != 2 or out.shape[0] != M:
         raise WedlmError(f"out: shape {tuple(out.shape)} is not [{M}, >= {N}]")
+    need = wedlm_linear_workspace_size(M, N, K, epilogue)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
     code = _load().wedlm_linear(
         _t(x, "x", _BF16), _t(w, "w", _BF16, (rows, K)), M, N, K,
-        int(epilogue), _t(out, "out", odt), out.shape[1], _stream())
+        int(epilogue), _t(out, "out", odt), out.shape[1],
+        None if workspace is None else workspace.data_ptr(),
+        0 if workspace is None else workspace.numel(), _stream())
     _check(code, "wedlm_linear")
 
 
@@ -558,7 +599,10 @@ class Decoder:
     """A decoder's device state for B sequences and the two calls of one
     streaming step (wedlm_model_forward, wedlm_commit_layers).
 
-    weights: dict of bf16 device tensors (WEIGHT_NAMES, weight_shapes()).
+    weights: dict of bf16 device tensors (WEIGHT_NAMES, weight_shapes()),
+    all row-major unless packed=True says the projections (PACKED) are
+    already in the layout of wedlm_pack_weights; row-major ones are packed
+    here into copies.
     Caches: [L, num_pages, ...]; each sequence owns the pages its block-table
     row lists.  The window state (win_tok, win_start) lives here and is
     updated in place by step()."""
@@ -566,8 +610,12 @@ class Decoder:
     def __init__(self, cfg: ModelConfig, weights: dict, B: int, W: int,
                  num_pages: int, block_table, max_prefix_len: int,
                  tau=0.9, lam=0.01, temperature=0.1, rule="stream",
-                 device="cuda"):
+                 device="cuda", packed=False):
         self.cfg, self.B, self.W = cfg, B, W
+        if not packed:
+            weights = dict(weights)
+            for n in PACKED:
+                weights[n] = pack(weights[n])
         self.tensors = weights
         self.weights = model_weights(cfg, weights)
         self.tau, self.lam, self.temperature = tau, lam, temperature

@@ -173,11 +173,19 @@ def test_model_workspace_and_config_checks():
 def test_linear_and_small_kernels_reject_bad_arguments():
     lib = _lib()
     f = _fake()
-    assert lib.wedlm_linear(f, f, 4, 48, 256, 0, f, 48, None) == -2  # N%32
-    assert lib.wedlm_linear(f, f, 4, 64, 200, 0, f, 64, None) == -2  # K%64
-    assert lib.wedlm_linear(f, f, 4, 64, 256, 3, f, 64, None) == -1  # epi
-    assert lib.wedlm_linear(f, f, 4, 64, 256, 0, f, 32, None) == -2  # ldo<N
-    assert lib.wedlm_linear(None, f, 4, 64, 256, 0, f, 64, None) == -1
+    lin = lambda *a: lib.wedlm_linear(*a, None, 0, None)
+    assert lin(f, f, 4, 48, 256, 0, f, 48) == -2      # N % 32
+    assert lin(f, f, 4, 64, 200, 0, f, 64) == -2      # K % 64
+    assert lin(f, f, 4, 64, 256, 3, f, 64) == -1      # epilogue
+    assert lin(f, f, 4, 64, 256, 0, f, 32) == -2      # ldo < N
+    assert lin(None, f, 4, 64, 256, 0, f, 64) == -1
+    # N = 4096 at 32 rows splits K over workgroups: a workspace is needed
+    need = lib.wedlm_linear_workspace_size(32, 4096, 4096, 1)
+    assert need > 0
+    assert lin(f, f, 32, 4096, 4096, 1, f, 4096) == -3
+    assert lib.wedlm_linear(f, f, 32, 4096, 4096, 1, f, 4096, f, need - 1,
+                            None) == -3
+    assert lib.wedlm_linear_workspace_size(32, 48, 256, 0) == 0
     assert lib.wedlm_rmsnorm(f, f, 4, 256, 0.0, f, None) == -1       # eps
     assert lib.wedlm_rmsnorm(f, f, 4, 254, 1e-6, f, None) == -2
     assert lib.wedlm_embed(f, 4, 1000, f, 1000, 256, f, None) == -2  # mask id

@@ -122,6 +122,25 @@ def test_qk_norm_rope(M, Hq, Hkv, D):
                           qkv.reshape(M, Hq + 2 * Hkv, D)[:, Hq + Hkv:])
 
 
+def test_pack_layout_exact():
+    """The packed tile layout of include/wedlm_model.h, element by element."""
+    w = W_()
+    rows, K = 96, 192
+    src = np.arange(rows * K, dtype=np.uint16).reshape(rows, K)
+    got = w.pack(_bf(src)).cpu().view(torch.int16).numpy().view(np.uint16)
+    got = got.reshape(-1)
+    S = K // 64
+    for r in range(rows // 32):
+        for s in range(S):
+            base = (r * S + s) * 2048
+            for j in range(4):
+                for l in range(64):
+                    k0 = 64 * s + 32 * (l // 32) + 8 * j
+                    e = base + (j * 64 + l) * 8
+                    assert np.array_equal(got[e:e + 8],
+                                          src[32 * r + l % 32, k0:k0 + 8])
+
+
 LINEAR_CASES = [
     # M, N, K
     (1, 32, 64), (5, 96, 256), (32, 256, 4096), (33, 64, 512),
@@ -147,7 +166,7 @@ def test_linear(M, N, K, epi):
     else:
         out = torch.full((M, ldo), float("nan"), dtype=torch.bfloat16,
                          device=DEV)
-    w.wedlm_linear(_bf(x), _bf(wt), epi, out)
+    w.wedlm_linear(_bf(x), w.pack(_bf(wt)), epi, out)
     torch.cuda.synchronize()
     got = _f64(out)
     if epi == 0:
@@ -167,6 +186,29 @@ def test_linear(M, N, K, epi):
                np.abs(MO.silu(g)) * eu + 1e-6 * np.abs(ref) + 1e-30)
         err = np.abs(got - ref)
         assert (err <= tol).all(), err.max()
+
+
+def test_linear_split_workspace_reuse():
+    """Products that split K over workgroups (residual add at N = 4096) share
+    one workspace back to back with products that do not."""
+    w = W_()
+    rng = np.random.default_rng(11)
+    need = max(w.wedlm_linear_workspace_size(32, 4096, 4096, 1),
+               w.wedlm_linear_workspace_size(32, 256, 4096, 0))
+    ws = torch.zeros(need, dtype=torch.uint8, device=DEV)
+    for (N, epi) in ((4096, 1), (256, 0), (4096, 1)):
+        x = _rand_bf16(rng, (32, 4096))
+        wt = _rand_bf16(rng, (N, 4096), 1 / 64)
+        out = (torch.zeros(32, N, dtype=torch.float32, device=DEV) if epi
+               else torch.empty(32, N, dtype=torch.bfloat16, device=DEV))
+        w.wedlm_linear(_bf(x), w.pack(_bf(wt)), epi, out, workspace=ws)
+        torch.cuda.synchronize()
+        prod = O.bf16_to_f64(x) @ O.bf16_to_f64(wt).T
+        bound = 4096 * 2.0 ** -24 * (np.abs(O.bf16_to_f64(x)) @
+                                     np.abs(O.bf16_to_f64(wt)).T)
+        err = np.abs(_f64(out) - prod)
+        assert (err <= 2.0 ** -8 * np.abs(prod) * (epi == 0) + bound +
+                1e-30).all()
 
 
 # ---------------------------------------------------------------------------
@@ -313,3 +355,49 @@ def test_decoder_graph_replay_matches_eager():
             assert np.array_equal(x, y, equal_nan=True)
     assert torch.equal(k0.view(torch.int16), k1.view(torch.int16))
     assert torch.equal(v0.view(torch.int16), v1.view(torch.int16))
+
+
+def test_qwen3_shaped_layer_against_oracle():
+    """One layer at the Qwen3-8B sizes (hidden 4096, 32/8 heads of 128, MLP
+    12288; vocabulary cut to 4096), two sequences of W = 32: 64 rows, so the
+    residual-add products split K over workgroups and the RMSNorms sum the
+    split partials.  Prefill of 64 prompt tokens, then two streaming steps
+    checked against the full-sequence oracle as in the tiny decoder test."""
+    ms = WL.ModelShape("qwen3_8b_1l_v4k", 302, L=1, Hd=4096, Hq=32, Hkv=8,
+                       D=128, I=12288, V=4096)
+    B, W, c0, T = 2, 32, 64, 1.0
+    wbits = WL.model_weights(ms, seed=0)
+    wf = MO.decode(wbits)
+    dec, bt = _decoder(ms, wbits, B, W, pages_per_seq=10, T=T)
+    prompt = WL.model_prompt(ms, B, c0, seed=5)
+    _prefill(dec, prompt)
+    y = [list(prompt[b]) for b in range(B)]
+    compared = 0
+    for t in range(2):
+        win = dec.win_tok.cpu().numpy().copy()
+        c = dec.win_start.cpu().numpy().copy()
+        dec.forward()
+        torch.cuda.synchronize()
+        am = dec.argmax.cpu().numpy()
+        H = dec.entropy.cpu().numpy()
+        kw = _f64(dec.k_win)
+        for b in range(B):
+            r = MO.window_scores(ms, wf, y[b], list(win[b]), T)
+            for i in range(r["n_obs"], W):
+                lg = np.sort(r["logits"][i])
+                assert abs(H[b, i] - r["H"][i]) < 0.03, (t, b, i)
+                if lg[-1] - lg[-2] > 0.05:
+                    assert am[b, i] == r["tok"][i], (t, b, i)
+                    compared += 1
+            kref = r["k"][:, c[b] + np.asarray(r["perm"])]
+            assert np.abs(kw[:, b] - kref).max() < 0.02 * np.abs(kref).max()
+        exp = [O.commit(list(win[b]), int(c[b]), list(H[b].astype(np.float64)),
+                        list(am[b]), dec.tau, dec.lam, list(bt[b]))
+               for b in range(B)]
+        dec.commit()
+        torch.cuda.synchronize()
+        for b in range(B):
+            assert int(dec.n_commit[b]) == exp[b]["n"]
+            assert list(dec.win_tok[b].cpu().numpy()) == exp[b]["win"]
+            y[b] += exp[b]["committed"]
+    assert compared > 10
