@@ -217,6 +217,8 @@ def bench_model(args, dev):
     w_bytes = sum(t.numel() * 2 for n, t in tens.items() if n != "embed")
     W = 32
     for B, c0 in ((1, 2048), (16, 1024)):
+        if args.model_batch and B != args.model_batch:
+            continue
         steps, warm = args.steps, args.warmup
         per = -(-(c0 + (steps + warm + 2) * W) // 16)
         bt = torch.arange(B * per, dtype=torch.int32,
@@ -387,6 +389,8 @@ def main():
                     help="time the Qwen3-8B-shaped decoder step, then exit")
     ap.add_argument("--model-layers", type=int, default=0,
                     help="layers of --model (default: 36)")
+    ap.add_argument("--model-batch", type=int, default=0,
+                    help="only this batch of --model (1 or 16)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for "
                          "scaling HBM counters) and exit")

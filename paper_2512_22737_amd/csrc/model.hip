@@ -37,6 +37,17 @@ using namespace wedlm;
 
 namespace {
 
+constexpr int kKStep = 64;                        // k per MFMA step (4 x 16)
+
+// Element (t, k) of an activation matrix with K columns in the packed tile
+// layout (the weights' layout applied to rows of tokens): tile (t/32, k/64)
+// at 2048 * (t/32 * K/64 + k/64), lane t%32 + 32 * (k%64 / 32), MFMA j =
+// k%32 / 8, element k%8.
+__device__ __forceinline__ int64_t tile_off(int64_t t, int k, int K) {
+  return ((t / 32 * (K / kKStep) + k / kKStep) * 4 + (k & 31) / 8) * 512 +
+         ((t & 31) + 32 * ((k & 63) / 32)) * 8 + (k & 7);
+}
+
 // ---------------------------------------------------------------------------
 // embedding: x[t] = E[token], [M] -> the mask row; fp32 residual stream
 // ---------------------------------------------------------------------------
@@ -71,7 +82,7 @@ __global__ __launch_bounds__(256) void embed_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kNormThreads = 256;
 
-template <bool ADD>
+template <bool ADD, bool XP>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
     float* __restrict__ x, const float* __restrict__ part, int n_ks, int M,
     const uint16_t* __restrict__ g, int Hd, float eps,
@@ -101,7 +112,7 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
 #pragma unroll
   for (int i = 0; i < kNormThreads / kWave; ++i) tot += wsum[i];
   const float r = 1.0f / sqrtf(tot / static_cast<float>(Hd) + eps);
-  uint16_t* out = y + static_cast<int64_t>(t) * Hd;
+  uint16_t* out = y + static_cast<int64_t>(t) * Hd;   // row-major
   // every thread re-reads only the chunks it wrote itself
   for (int c = threadIdx.x; c < Hd / 4; c += kNormThreads) {
     const floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
@@ -109,7 +120,8 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
     u16x4_t o;
 #pragma unroll
     for (int e = 0; e < 4; ++e) o[e] = f32_to_bf16(v[e] * r * bf16_to_f32(gg[e]));
-    *reinterpret_cast<u16x4_t*>(out + c * 4) = o;
+    // packed (XP): the 4 values share one 16-byte chunk of a tile
+    *reinterpret_cast<u16x4_t*>(XP ? y + tile_off(t, c * 4, Hd) : out + c * 4) = o;
   }
 }
 
@@ -196,7 +208,6 @@ __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kGWaves = 8;
 constexpr int kGThreads = kGWaves * kWave;
-constexpr int kKStep = 64;
 constexpr int kRedStride = 33;                    // LDS row of 32 tokens + 1
 
 enum Epi { kStoreBf16 = 0, kAddF32 = 1, kSwiglu = 2 };
@@ -214,21 +225,31 @@ struct GemmArgs {
   float* part;            // n_ks > 1: [n_ks, M, N] partial products
 };
 
-template <int EPI>
-__device__ __forceinline__ void gemm_store(const GemmArgs& a, int64_t o,
+// XP: the SwiGLU output is written in the packed tile layout (the next
+// product's input)
+template <int EPI, bool XP>
+__device__ __forceinline__ void gemm_store(const GemmArgs& a, int tok, int n,
                                            float g, float u) {
+  const int64_t o = static_cast<int64_t>(tok) * a.ldo + n;
   if constexpr (EPI == kStoreBf16) {
     static_cast<uint16_t*>(a.out)[o] = f32_to_bf16(g);
   } else if constexpr (EPI == kAddF32) {
     static_cast<float*>(a.out)[o] += g;
   } else {
-    static_cast<uint16_t*>(a.out)[o] = f32_to_bf16(g / (1.0f + expf(-g)) * u);
+    const uint16_t r = f32_to_bf16(g / (1.0f + expf(-g)) * u);
+    if constexpr (XP)
+      static_cast<uint16_t*>(a.out)[tile_off(tok, n, a.N)] = r;
+    else
+      static_cast<uint16_t*>(a.out)[o] = r;
   }
 }
 
 // NT: weight loads carry the non-temporal hint (one row group; with several,
-// the groups share the weight lines through L2)
-template <int NB, int NA, int PF, int EPI, bool NT>
+// the groups share the weight lines through L2).  XP: the activations come
+// in the packed tile layout (ceil(M/32) tiles of 32 rows; rows past M are
+// never stored), so each activation load is 1 KB of contiguous memory too;
+// otherwise row-major, 64 contiguous bytes of a token row per lane and step.
+template <int NB, int NA, int PF, int EPI, bool NT, bool XP>
 __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
   constexpr int RB = 32 * NB;
   constexpr int TPC = 2;                            // tiles per LDS round
@@ -274,8 +295,13 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
     const uint16_t* xrow[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      const int t = min(rg * RB + b * 32 + col, a.M - 1);
-      xrow[b] = a.x + static_cast<int64_t>(t) * a.K + hf * 32 + s0 * kKStep;
+      if constexpr (XP) {
+        const int tb = min(rg * NB + b, (a.M - 1) / 32);
+        xrow[b] = a.x + (static_cast<int64_t>(tb) * S + s0) * kTile + lane * 8;
+      } else {
+        const int t = min(rg * RB + b * 32 + col, a.M - 1);
+        xrow[b] = a.x + static_cast<int64_t>(t) * a.K + hf * 32 + s0 * kKStep;
+      }
     }
     u16x8_t wa[PF][NA][4], xb[PF][NB][4];
     // every load is issued (steps past the run re-read its last step), so
@@ -297,8 +323,8 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
       for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-          rb[b][u] = *reinterpret_cast<const u16x8_t*>(xrow[b] + qq * kKStep +
-                                                       u * 8);
+          rb[b][u] = *reinterpret_cast<const u16x8_t*>(
+              XP ? xrow[b] + qq * kTile + u * 512 : xrow[b] + qq * kKStep + u * 8);
     };
     auto mfma = [&](const u16x8_t (&ra)[NA][4], const u16x8_t (&rb)[NB][4]) {
 #pragma unroll
@@ -368,8 +394,7 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
         }
         if (tok >= a.M) continue;
         if (a.n_ks == 1) {
-          gemm_store<EPI>(a, static_cast<int64_t>(tok) * a.ldo + nb * 32 + f,
-                          v[0], v[NA - 1]);
+          gemm_store<EPI, XP>(a, tok, nb * 32 + f, v[0], v[NA - 1]);
         } else {
           // split K (residual add): this split's partial, summed into the
           // residual stream later in split order
@@ -421,18 +446,24 @@ int gemm_nb(int M, bool swiglu) {
 
 // the largest row block of each kernel family also serves several row
 // groups; the smaller ones only ever run as one
-template <int NB, int NA, int PF, int EPI>
-void gemm_launch(const GemmArgs& a, hipStream_t st) {
+template <int NB, int NA, int PF, int EPI, bool XP>
+void gemm_launch_xp(const GemmArgs& a, hipStream_t st) {
   const int64_t grid = 8ll * a.n_rg * a.n_ks * ((a.n_nb + 7) / 8);
   if constexpr (NB * NA == 4) {
     if (a.n_rg > 1) {
-      hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, false>), dim3(grid),
+      hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, false, XP>), dim3(grid),
                          dim3(kGThreads), 0, st, a);
       return;
     }
   }
-  hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, true>), dim3(grid),
+  hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, true, XP>), dim3(grid),
                      dim3(kGThreads), 0, st, a);
+}
+
+template <int NB, int NA, int PF, int EPI>
+void gemm_launch(const GemmArgs& a, bool xp, hipStream_t st) {
+  if (xp) gemm_launch_xp<NB, NA, PF, EPI, true>(a, st);
+  else gemm_launch_xp<NB, NA, PF, EPI, false>(a, st);
 }
 
 bool gemm_shape_ok(int M, int N, int K) {
@@ -473,8 +504,9 @@ GemmPlan gemm_plan(int M, int N, int K, int epi) {
 
 // Launches the product; with K split, the partials go to `part` and the
 // caller adds them (defer) or add_partials_kernel does right after.
+// xp: x (and a SwiGLU output) in the packed tile layout
 int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
-         int ldo, int epi, void* part, size_t part_bytes, bool defer,
+         int ldo, int epi, void* part, size_t part_bytes, bool defer, bool xp,
          hipStream_t st, int* n_ks_out = nullptr) {
   if (!x || !w || !out) return WEDLM_E_ARG;
   if (epi != kStoreBf16 && epi != kAddF32 && epi != kSwiglu) return WEDLM_E_ARG;
@@ -493,16 +525,16 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
     return WEDLM_E_SHAPE;
   const int nb = p.nb;
   if (epi == kSwiglu) {
-    if (nb == 1) gemm_launch<1, 2, 2, kSwiglu>(a, st);
-    else gemm_launch<2, 2, 2, kSwiglu>(a, st);
+    if (nb == 1) gemm_launch<1, 2, 2, kSwiglu>(a, xp, st);
+    else gemm_launch<2, 2, 2, kSwiglu>(a, xp, st);
   } else if (epi == kAddF32) {
-    if (nb == 1) gemm_launch<1, 1, 4, kAddF32>(a, st);
-    else if (nb == 2) gemm_launch<2, 1, 2, kAddF32>(a, st);
-    else gemm_launch<4, 1, 2, kAddF32>(a, st);
+    if (nb == 1) gemm_launch<1, 1, 4, kAddF32>(a, xp, st);
+    else if (nb == 2) gemm_launch<2, 1, 2, kAddF32>(a, xp, st);
+    else gemm_launch<4, 1, 2, kAddF32>(a, xp, st);
   } else {
-    if (nb == 1) gemm_launch<1, 1, 4, kStoreBf16>(a, st);
-    else if (nb == 2) gemm_launch<2, 1, 2, kStoreBf16>(a, st);
-    else gemm_launch<4, 1, 2, kStoreBf16>(a, st);
+    if (nb == 1) gemm_launch<1, 1, 4, kStoreBf16>(a, xp, st);
+    else if (nb == 2) gemm_launch<2, 1, 2, kStoreBf16>(a, xp, st);
+    else gemm_launch<4, 1, 2, kStoreBf16>(a, xp, st);
   }
   WEDLM_LAUNCH_CHECK();
   if (n_ks_out) *n_ks_out = p.n_ks;
@@ -516,15 +548,15 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
   return WEDLM_OK;
 }
 
-// RMSNorm of the residual stream, first adding pending split partials
+// RMSNorm of the residual stream, first adding pending split partials; xp:
+// y in the packed tile layout (Hd a multiple of 64)
 int norm(float* x, const float* part, int n_ks, int M, int Hd,
-         const uint16_t* g, float eps, uint16_t* y, hipStream_t st) {
-  if (part && n_ks > 1)
-    hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(M), dim3(kNormThreads), 0,
-                       st, x, part, n_ks, M, g, Hd, eps, y);
-  else
-    hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(M), dim3(kNormThreads), 0,
-                       st, x, nullptr, 0, M, g, Hd, eps, y);
+         const uint16_t* g, float eps, uint16_t* y, bool xp, hipStream_t st) {
+  const bool add = part && n_ks > 1;
+  auto k = add ? (xp ? rmsnorm_kernel<true, true> : rmsnorm_kernel<true, false>)
+               : (xp ? rmsnorm_kernel<false, true> : rmsnorm_kernel<false, false>);
+  hipLaunchKernelGGL(k, dim3(M), dim3(kNormThreads), 0, st, x,
+                     add ? part : nullptr, add ? n_ks : 0, M, g, Hd, eps, y);
   WEDLM_LAUNCH_CHECK();
   return WEDLM_OK;
 }
@@ -559,11 +591,12 @@ Carve carve(const wedlm_model_config* c, int B, int W, int max_prefix_len) {
       gemm_plan(Mi, c->hidden, c->inter, kAddF32).part_bytes);
   k.part = off; off += up256(k.part_bytes);
   k.x = off;    off += up256(M * Hd * 4);
-  k.xn = off;   off += up256(M * Hd * 2);
+  const size_t Mp = (M + 31) / 32 * 32;           // packed: whole tiles
+  k.xn = off;   off += up256(Mp * Hd * 2);
   k.qkv = off;  off += up256(M * (Hq + 2 * Hkv) * D * 2);
   k.q = off;    off += up256(M * Hq * D * 2);
   k.attn = off; off += up256(M * Hq * D * 2);
-  k.act = off;  off += up256(M * c->inter * 2);
+  k.act = off;  off += up256(Mp * c->inter * 2);
   k.attn_ws = off;
   off += up256(wedlm_window_attn_workspace_size(B, W, c->n_heads,
                                                 c->n_kv_heads, c->head_dim,
@@ -601,7 +634,7 @@ extern "C" int wedlm_rmsnorm(const float* x, const uint16_t* gain, int32_t M,
   if (!x || !gain || !y || !(eps > 0.f)) return WEDLM_E_ARG;
   if (M < 1 || Hd < 4 || Hd % 4 != 0) return WEDLM_E_SHAPE;
   // without partials the kernel only reads x
-  return norm(const_cast<float*>(x), nullptr, 0, M, Hd, gain, eps, y,
+  return norm(const_cast<float*>(x), nullptr, 0, M, Hd, gain, eps, y, false,
               static_cast<hipStream_t>(stream));
 }
 
@@ -633,7 +666,7 @@ extern "C" int wedlm_linear(const uint16_t* x, const uint16_t* w, int32_t M,
                             int32_t ldo, void* workspace,
                             size_t workspace_bytes, void* stream) {
   return gemm(x, w, M, N, K, out, ldo, epilogue, workspace, workspace_bytes,
-              false, static_cast<hipStream_t>(stream));
+              false, false, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int wedlm_qk_norm_rope(const uint16_t* qkv, const uint16_t* q_gain,
@@ -727,9 +760,9 @@ extern "C" int wedlm_model_forward(
     uint16_t* vl = v_win + l * win_stride;
     WEDLM_TRY(norm(x, part, pend, M, Hd,
                    wt->attn_norm + static_cast<int64_t>(l) * Hd, cfg->rms_eps,
-                   xn, st));
+                   xn, true, st));
     WEDLM_TRY(gemm(xn, wt->w_qkv + static_cast<int64_t>(l) * QKV * Hd, M, QKV,
-                   Hd, qkv, QKV, kStoreBf16, nullptr, 0, true, st));
+                   Hd, qkv, QKV, kStoreBf16, nullptr, 0, true, true, st));
     WEDLM_TRY(wedlm_qk_norm_rope(qkv, wt->q_norm + static_cast<int64_t>(l) * D,
                                  wt->k_norm + static_cast<int64_t>(l) * D,
                                  pos_ids, M, Hq, Hkv, D, cfg->rope_theta,
@@ -740,17 +773,19 @@ extern "C" int wedlm_model_forward(
         max_prefix_len, scale, attn, nullptr, status, attn_ws, attn_ws_bytes,
         stream));
     WEDLM_TRY(gemm(attn, wt->w_o + static_cast<int64_t>(l) * Hd * Hq * D, M,
-                   Hd, Hq * D, x, Hd, kAddF32, part, part_bytes, true, st,
-                   &pend));
+                   Hd, Hq * D, x, Hd, kAddF32, part, part_bytes, true, false,
+                   st, &pend));
     WEDLM_TRY(norm(x, part, pend, M, Hd,
                    wt->mlp_norm + static_cast<int64_t>(l) * Hd, cfg->rms_eps,
-                   xn, st));
+                   xn, true, st));
     WEDLM_TRY(gemm(xn, wt->w_gate_up + static_cast<int64_t>(l) * 2 * I * Hd, M,
-                   I, Hd, act, I, kSwiglu, nullptr, 0, true, st));
+                   I, Hd, act, I, kSwiglu, nullptr, 0, true, true, st));
     WEDLM_TRY(gemm(act, wt->w_down + static_cast<int64_t>(l) * Hd * I, M, Hd,
-                   I, x, Hd, kAddF32, part, part_bytes, true, st, &pend));
+                   I, x, Hd, kAddF32, part, part_bytes, true, true, st,
+                   &pend));
   }
-  WEDLM_TRY(norm(x, part, pend, M, Hd, wt->final_norm, cfg->rms_eps, xn, st));
+  WEDLM_TRY(norm(x, part, pend, M, Hd, wt->final_norm, cfg->rms_eps, xn, false,
+                 st));
   WEDLM_TRY(wedlm_lm_head_score(xn, wt->lm_head, M, Hd, cfg->vocab,
                                 temperature, argmax, entropy, pmax, lm_ws,
                                 lm_ws_bytes, stream));

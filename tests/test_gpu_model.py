@@ -247,8 +247,11 @@ def _prefill(dec, prompt):
     assert (dec.win_tok.cpu().numpy() == O.MASK).all()
 
 
-def test_decoder_streaming_steps_against_oracle():
-    B, W, c0, steps, T = 2, 16, 32, 6, 1.0
+@pytest.mark.parametrize("B,W", [(2, 16), (3, 12)])
+def test_decoder_streaming_steps_against_oracle(B, W):
+    """(2, 16): 32 window rows, one row tile; (3, 12): 36 rows, a ragged
+    second tile in the packed activations."""
+    c0, steps, T = 2 * W, 6, 1.0
     wbits = WL.model_weights(MS, seed=0)
     wf = MO.decode(wbits)
     dec, bt = _decoder(MS, wbits, B, W, pages_per_seq=12, T=T)
