@@ -30,6 +30,10 @@ What it computes, following WeDLM (arXiv 2512.22737):
   lm_head_score  The logits of the forward's output layer (hidden states
                times the vocabulary matrix) scored as above, for the fused
                LM-head kernel.
+  dual_stream_*  The training-time attention of Sec. 4.2: a clean memory
+               stream followed by the block-wise reordered prediction
+               stream, with the block attention pattern written out as a
+               dense mask (masked_attention).
 
 Readings where the paper is silent or loose (each is listed with its reason
 in the design notes of the repository):
@@ -54,6 +58,10 @@ in the design notes of the repository):
     as streaming, but nothing is committed while any slot of the block is a
     mask; the step that sees the whole block filled commits all W slots and
     the window refills with W masks (Fig. 3 "stop-and-wait", Sec. 6.4).
+  * Dual-stream attention: the memory stream is causal over itself (it is
+    the clean sequence); block k of the prediction stream sees memory
+    positions < kB and its own reordered block causally, itself included;
+    both streams carry the logical positions 0..L-1 (Eq. 8).
   * One-token rule: exactly one mask per step, the one with the smallest
     H_i + lambda * d_i (ties: leftmost), whatever tau; commit as in
     streaming (Sec. 6.2's unified step-wise scheme).
@@ -449,3 +457,69 @@ def p_cache(n_hist: np.ndarray, W: int) -> float:
     (each step forwards W window tokens per sequence)."""
     steps, B = n_hist.shape
     return float(n_hist.sum()) / float(steps * B * W)
+
+
+# --------------------------------------------------------------------------
+# Sec. 4.2: dual-stream masking (training forward of the attention)
+# --------------------------------------------------------------------------
+
+def dual_stream_order(L: int, B: int, masked):
+    """Physical layout of Eq. (7)'s input: the memory stream (logical
+    positions 0..L-1 in order), then the prediction stream cut into blocks of
+    B, each block reordered as in Sec. 4.1 (its observed positions first,
+    then its masked ones, each group ascending).  masked: set of masked
+    logical positions of the prediction stream.  Returns a list of
+    (stream, logical position, masked) per physical row, stream 0 = memory,
+    1 = prediction."""
+    rows = [(0, p, False) for p in range(L)]
+    for b0 in range(0, L, B):
+        blk = list(range(b0, min(b0 + B, L)))
+        obs = [p for p in blk if p not in masked]
+        msk = [p for p in blk if p in masked]
+        rows += [(1, p, False) for p in obs] + [(1, p, True) for p in msk]
+    return rows
+
+
+def dual_stream_visible(L: int, B: int, masked):
+    """vis[i, j] for the physical rows of dual_stream_order, written from the
+    attention pattern of Sec. 4.2: a memory token sees earlier-or-equal
+    memory tokens (the clean causal stream); a prediction token in block k
+    sees the memory tokens whose logical positions precede block k and the
+    tokens of its own reordered block that physically precede it (itself
+    included); nothing else."""
+    rows = dual_stream_order(L, B, masked)
+    n = len(rows)
+    vis = np.zeros((n, n), dtype=bool)
+    for i, (si, pi, _) in enumerate(rows):
+        ki = pi // B
+        for j, (sj, pj, _) in enumerate(rows):
+            if si == 0:
+                vis[i, j] = sj == 0 and pj <= pi
+            elif sj == 0:
+                vis[i, j] = pj < ki * B
+            else:
+                vis[i, j] = pj // B == ki and j <= i
+    return vis
+
+
+def masked_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
+                     vis: np.ndarray):
+    """softmax(q k^T / sqrt(D) restricted to vis) v for every row and head.
+    q [n, Hq, D], k and v [n, Hkv, D] (rotated q and k), GQA h -> h // G.
+    Returns out [n, Hq, D] and lse [n, Hq] (natural log)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    n, Hq, D = q.shape
+    G = Hq // k.shape[1]
+    out = np.zeros((n, Hq, D))
+    lse = np.zeros((n, Hq))
+    for h in range(Hq):
+        s = (q[:, h] @ k[:, h // G].T) / math.sqrt(D)
+        s = np.where(vis, s, -np.inf)
+        m = s.max(axis=1, keepdims=True)
+        p = np.exp(s - m)
+        z = p.sum(axis=1, keepdims=True)
+        out[:, h] = (p / z) @ v[:, h // G]
+        lse[:, h] = (m + np.log(z))[:, 0]
+    return out, lse
