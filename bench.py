@@ -30,6 +30,12 @@ replayed.  One JSON line per batch: ms per step, window tokens/s, committed
 tokens/s, p_cache, and the step's HBM roofline (weights + the caches' keys
 and values read per step, over the step time, against 8 TB/s).
 
+--dual-stream instead times the training-time attention of Sec. 4.2
+(wedlm_dual_stream_attn: clean memory stream + block-reordered prediction
+stream, blocks of 32) at the Qwen3-8B heads (32/8 of 128) for 4 sequences of
+4096 tokens, and prints its MFMA roofline (the flops of the visible
+query-key pairs over the time, against 2.5 PFLOP/s).
+
 --compare-rules instead runs the streaming workload (16 sequences, starting
 prefix 1024, W=32, V=151936, fresh synthetic logits every step) under each
 decoding rule of wedlm_commit_rule (Algorithm 1's streaming commit,
@@ -295,6 +301,43 @@ def bench_model(args, dev):
         torch.cuda.synchronize()
 
 
+def bench_dual_stream(args, dev):
+    import torch
+    from paper_2512_22737_amd import wedlm
+    n_seq, L, B, Hq, Hkv, D = 4, 4096, 32, 32, 8, 128
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed)
+    mk = lambda h: torch.randn((n_seq, 2 * L, h, D), generator=g, device=dev,
+                               dtype=torch.bfloat16)
+    q, k, v = mk(Hq), mk(Hkv), mk(Hkv)
+    out = torch.empty_like(q)
+    ws = torch.empty(wedlm.wedlm_dual_stream_attn_workspace_size(
+        n_seq, L, B, Hq, Hkv, D), dtype=torch.uint8, device=dev)
+    run = lambda: wedlm.wedlm_dual_stream_attn(q, k, v, B, out, workspace=ws)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    K = L // B
+    pairs = L * (L + 1) // 2 + B * B * K * (K - 1) // 2 + K * B * (B + 1) // 2
+    flops = 4.0 * D * Hq * pairs * n_seq          # QK^T and PV
+    tf = flops / us / 1e6
+    print(json.dumps({
+        "kind": "dual_stream_attn", "n_seq": n_seq, "L": L, "block": B,
+        "Hq": Hq, "Hkv": Hkv, "D": D, "us": us, "flops": flops,
+        "tokens_per_s": n_seq * 2 * L / (us * 1e-6),
+        "roofline": {"bound": "mfma", "achieved": tf,
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tf / MFMA_BF16_PEAK_TFLOPS}}), flush=True)
+
+
 def compare_rules(args, dev):
     """Decoding rules on the streaming workload: every run starts from the
     same all-mask windows at prefix 1024 and draws the same per-step logits
@@ -391,6 +434,8 @@ def main():
                     help="layers of --model (default: 36)")
     ap.add_argument("--model-batch", type=int, default=0,
                     help="only this batch of --model (1 or 16)")
+    ap.add_argument("--dual-stream", action="store_true",
+                    help="time the dual-stream training attention, then exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for "
                          "scaling HBM counters) and exit")
@@ -428,6 +473,9 @@ def main():
         return
     if args.model:
         bench_model(args, dev)
+        return
+    if args.dual_stream:
+        bench_dual_stream(args, dev)
         return
 
     wl = WL.WORKLOADS[args.workload]

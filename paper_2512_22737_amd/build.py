@@ -20,7 +20,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libwedlm.so")
 
 SOURCES = ["reorder.hip", "window_attn.hip", "score.hip", "commit.hip",
-           "lm_head.hip", "model.hip", "abi.hip"]
+           "lm_head.hip", "model.hip", "dual_stream.hip", "abi.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -1,4 +1,5 @@
-"""Thin Python binding of libwedlm.so (include/wedlm.h, include/wedlm_model.h).
+"""Thin Python binding of libwedlm.so (include/wedlm.h, include/wedlm_model.h,
+include/wedlm_train.h).
 
 Argument marshalling only: each function checks the tensors it is handed
 (device, dtype, contiguity, shape), reads the sizes off them and calls the C
@@ -92,6 +93,11 @@ def _load():
                                         P, I32, I32, I32, I32, I32, I32, P, P,
                                         P, P, P, I32, P]
     lib.wedlm_commit_layers.restype = ctypes.c_int
+    lib.wedlm_dual_stream_attn_workspace_size.argtypes = [I32] * 6
+    lib.wedlm_dual_stream_attn_workspace_size.restype = SZ
+    lib.wedlm_dual_stream_attn.argtypes = [P, P, P, I32, I32, I32, I32, I32,
+                                           I32, F, P, P, P, SZ, P]
+    lib.wedlm_dual_stream_attn.restype = ctypes.c_int
     lib.wedlm_strerror.argtypes = [ctypes.c_int]
     lib.wedlm_strerror.restype = ctypes.c_char_p
     lib.wedlm_version.argtypes = []
@@ -112,7 +118,8 @@ EXPORTED = ["wedlm_reorder", "wedlm_window_attn_workspace_size",
             "wedlm_linear", "wedlm_linear_workspace_size",
             "wedlm_pack_weights", "wedlm_qk_norm_rope",
             "wedlm_model_workspace_size",
-            "wedlm_model_forward", "wedlm_commit_layers"]
+            "wedlm_model_forward", "wedlm_commit_layers",
+            "wedlm_dual_stream_attn_workspace_size", "wedlm_dual_stream_attn"]
 
 # decoding rules of wedlm_commit_rule (include/wedlm.h)
 RULE_STREAMING, RULE_BLOCK, RULE_ONE_TOKEN = 0, 1, 2
@@ -669,3 +676,39 @@ class Decoder:
     def step(self):
         self.forward()
         self.commit()
+
+
+# ---------------------------------------------------------------------------
+# training-time attention (include/wedlm_train.h)
+# ---------------------------------------------------------------------------
+
+def wedlm_dual_stream_attn_workspace_size(n_seq, L, block, Hq, Hkv, D) -> int:
+    return int(_load().wedlm_dual_stream_attn_workspace_size(
+        n_seq, L, block, Hq, Hkv, D))
+
+
+def wedlm_dual_stream_attn(q, k, v, block: int, out, lse=None, workspace=None,
+                           softmax_scale: Optional[float] = None) -> None:
+    """q [n_seq, 2L, Hq, D], k, v [n_seq, 2L, Hkv, D] bf16 in the physical
+    layout of include/wedlm_train.h -> out [n_seq, 2L, Hq, D] bf16, lse
+    [n_seq, 2L, Hq] fp32 (optional).  A workspace is allocated here if none
+    is given."""
+    n_seq, L2, Hq, D = q.shape
+    Hkv = k.shape[2]
+    L = L2 // 2
+    if softmax_scale is None:
+        softmax_scale = 1.0 / math.sqrt(D)
+    need = wedlm_dual_stream_attn_workspace_size(n_seq, L, block, Hq, Hkv, D)
+    if need == 0:
+        raise WedlmError("unsupported dual-stream shape")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    code = _load().wedlm_dual_stream_attn(
+        _t(q, "q", _BF16, (n_seq, 2 * L, Hq, D)),
+        _t(k, "k", _BF16, (n_seq, 2 * L, Hkv, D)),
+        _t(v, "v", _BF16, (n_seq, 2 * L, Hkv, D)), n_seq, L, int(block), Hq,
+        Hkv, D, float(softmax_scale), _t(out, "out", _BF16, (n_seq, 2 * L, Hq, D)),
+        _t(lse, "lse", (torch.float32,), (n_seq, 2 * L, Hq), allow_none=True),
+        _t(workspace, "workspace", (torch.uint8,)), workspace.numel(),
+        _stream())
+    _check(code, "wedlm_dual_stream_attn")
