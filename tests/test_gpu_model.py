@@ -76,7 +76,7 @@ def test_embed_exact():
     assert np.array_equal(x.cpu().double().numpy(), ref)
 
 
-@pytest.mark.parametrize("M,Hd", [(1, 256), (7, 4096), (33, 1000)])
+@pytest.mark.parametrize("M,Hd", [(1, 256), (7, 4096), (33, 1000), (3, 8192)])
 def test_rmsnorm(M, Hd):
     w = W_()
     rng = np.random.default_rng(M)
