@@ -22,8 +22,8 @@ above it).
 
 --model instead runs the decoder around the step: a Qwen3-8B-shaped model
 (36 layers, hidden 4096, 32/8 heads of 128, MLP 12288, vocabulary 151936,
-random bf16 weights) on two batches, 1 sequence with a 2048-token prompt and
-16 sequences with 1024-token prompts, window W=32.  The prompt is prefilled
+random bf16 weights) on three batches, 1 and 4 sequences with 2048-token
+prompts and 16 sequences with 1024-token prompts, window W=32.  The prompt is prefilled
 through the window path itself (all-filled windows); then one streaming step
 (wedlm_model_forward + wedlm_commit_layers) is captured in a HIP graph and
 replayed.  One JSON line per batch: ms per step, window tokens/s, committed
@@ -222,7 +222,7 @@ def bench_model(args, dev):
         tens[name] = t
     w_bytes = sum(t.numel() * 2 for n, t in tens.items() if n != "embed")
     W = 32
-    for B, c0 in ((1, 2048), (16, 1024)):
+    for B, c0 in ((1, 2048), (4, 2048), (16, 1024)):
         if args.model_batch and B != args.model_batch:
             continue
         steps, warm = args.steps, args.warmup
@@ -433,7 +433,7 @@ def main():
     ap.add_argument("--model-layers", type=int, default=0,
                     help="layers of --model (default: 36)")
     ap.add_argument("--model-batch", type=int, default=0,
-                    help="only this batch of --model (1 or 16)")
+                    help="only this batch of --model (1, 4 or 16)")
     ap.add_argument("--dual-stream", action="store_true",
                     help="time the dual-stream training attention, then exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,

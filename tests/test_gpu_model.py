@@ -247,10 +247,11 @@ def _prefill(dec, prompt):
     assert (dec.win_tok.cpu().numpy() == O.MASK).all()
 
 
-@pytest.mark.parametrize("B,W", [(2, 16), (3, 12)])
+@pytest.mark.parametrize("B,W", [(2, 16), (3, 12), (17, 16)])
 def test_decoder_streaming_steps_against_oracle(B, W):
     """(2, 16): 32 window rows, one row tile; (3, 12): 36 rows, a ragged
-    second tile in the packed activations."""
+    second tile in the packed activations; (17, 16): 272 rows, the 2-D tiled
+    products (three row tiles of 128, the last mostly empty)."""
     c0, steps, T = 2 * W, 6, 1.0
     wbits = WL.model_weights(MS, seed=0)
     wf = MO.decode(wbits)
@@ -360,15 +361,17 @@ def test_decoder_graph_replay_matches_eager():
     assert torch.equal(v0.view(torch.int16), v1.view(torch.int16))
 
 
-def test_qwen3_shaped_layer_against_oracle():
+@pytest.mark.parametrize("B", [2, 8])
+def test_qwen3_shaped_layer_against_oracle(B):
     """One layer at the Qwen3-8B sizes (hidden 4096, 32/8 heads of 128, MLP
-    12288; vocabulary cut to 4096), two sequences of W = 32: 64 rows, so the
-    residual-add products split K over workgroups and the RMSNorms sum the
-    split partials.  Prefill of 64 prompt tokens, then two streaming steps
+    12288; vocabulary cut to 4096), B sequences of W = 32: 64 rows (the
+    split-K products, the RMSNorms summing split partials) or 256 rows (the
+    2-D tiled products, o's input packed, residual-add products split over
+    8 workgroups).  Prefill of 64 prompt tokens, then two streaming steps
     checked against the full-sequence oracle as in the tiny decoder test."""
     ms = WL.ModelShape("qwen3_8b_1l_v4k", 302, L=1, Hd=4096, Hq=32, Hkv=8,
                        D=128, I=12288, V=4096)
-    B, W, c0, T = 2, 32, 64, 1.0
+    W, c0, T = 32, 64, 1.0
     wbits = WL.model_weights(ms, seed=0)
     wf = MO.decode(wbits)
     dec, bt = _decoder(ms, wbits, B, W, pages_per_seq=10, T=T)
