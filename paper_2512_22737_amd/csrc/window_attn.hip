@@ -16,9 +16,10 @@
 //   so a lane holds 16 scores of ONE query column and the row max / sum
 //   need one cross-half exchange; each K or V operand read from LDS feeds
 //   QB MFMAs.  The transposed V page layout makes V^T rows contiguous.
-// Latency hiding: global loads run PF tiles ahead into a ring of register
-//   stages (tile t lives in stage t % PF), so about PF * 16 KB are in flight
-//   per workgroup; LDS holds a ring of six tiles, one barrier per two.
+// Latency hiding: tiles go straight from HBM into an LDS ring of eight
+//   tile slots (buffer loads with the LDS-destination bit, no register
+//   staging), issued six tiles ahead; the workgroup synchronises once per
+//   two tiles.
 // Softmax: log2 domain, running max raised only when a tile's max exceeds
 //   it by more than 8 (p <= 2^8 otherwise), so the O rescale is rare.
 // Split-K: the prefix is split so that the grid fills the CUs; partials
@@ -141,6 +142,32 @@ __device__ __forceinline__ int load_uniform(const int32_t* p, int idx) {
   return ((const_i32_t*)p)[idx];
 }
 
+// 16 bytes per lane from a raw buffer straight into LDS: lane l's data
+// lands at LDS byte lds_addr + 16*l (lds_addr is passed in M0).  Issued
+// through inline asm so the compiler does not guard every later LDS read
+// with a wait for these loads (it cannot tell which slot they write); the
+// kernel waits for them explicitly (wait_vmcnt) before the barrier that
+// publishes a slot.  The cache stream is read once, so the loads carry the
+// non-temporal hint.
+__device__ __forceinline__ void load_to_lds16(i32x4_t rsrc, int voff,
+                                              uint32_t lds_addr) {
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen nt lds"
+               :
+               : "v"(voff), "s"(rsrc), "{m0}"(lds_addr));
+}
+
+// Raw buffer resource (stride 0) over num_bytes at base.
+__device__ __forceinline__ i32x4_t buffer_rsrc(const void* base,
+                                               int num_bytes) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  i32x4_t r;
+  r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(p & 0xffffffffu));
+  r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>((p >> 32) & 0xffffu));
+  r[2] = num_bytes;
+  r[3] = kBufferFlags;
+  return r;
+}
+
 // s_waitcnt with only the vector-memory counter bounded by N.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -149,15 +176,15 @@ __device__ __forceinline__ void wait_vmcnt() {
                              (0xF << 8));
 }
 
-// Stage layout in LDS (bytes), one 32-key tile:
+// Layout of one 32-key tile in LDS (bytes).  The K halves of all slots
+// form one region and the V^T halves another, each at most 64 KB, so every
+// fragment read reaches any slot from one address register plus the
+// instruction's 16-bit offset.
 //   K   [32 keys][2D bytes]: 16-byte chunk c of key row r sits in slot
 //       c ^ swz_k(r), so the 16 lanes of one ds_read_b128 pass (16 rows,
 //       same chunk) hit 16 different slots.
 //   V^T [2 pages][D rows][32 bytes]: chunk c (8 keys) of row d sits in slot
 //       c ^ ((d >> 3) & 1); 16 lanes reading rows d..d+15 cover all banks.
-// Tiles arrive through register stages: each lane loads fixed 16-byte
-// chunks of the tile's four contiguous page blocks and writes each to its
-// swizzled slot with ds_write_b128.
 template <int D>
 struct Tile {
   static constexpr int kBytes = kTileKeys * D * 2;
@@ -174,11 +201,9 @@ struct Tile {
     return key * 2 * D + ((c ^ swz_k(key)) << 4);
   }
   __device__ static __forceinline__ int v_off(int h, int d, int c) {
-    return kBytes + h * D * 32 + d * 32 + ((c ^ ((d >> 3) & 1)) << 4);
+    return h * D * 32 + d * 32 + ((c ^ ((d >> 3) & 1)) << 4);
   }
 };
-
-constexpr int gcd_c(int x, int y) { return y == 0 ? x : gcd_c(y, x % y); }
 
 // Key row of the score tile held in MFMA output row m: bits 2 and 3 of m
 // swapped, so that output element e of a lane (hf = lane / 32) is key
@@ -187,14 +212,19 @@ __device__ __forceinline__ int key_of_row(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
 
-template <int D, int NW, int QB, int PF>
+template <int D, int NW, int QB>
 __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   using T = Tile<D>;
   constexpr int NK = D / 16;          // k-steps of the score MFMA
   constexpr int NM = D / 32;          // 32-row blocks of O^T
-  static_assert(PF >= 2, "register prefetch depth");
-  constexpr int NS = 6;               // LDS ring of 32-key tile slots
+  constexpr int NS = 8;               // LDS ring of 32-key tile slots
+  constexpr int LEAD = NS - 2;        // tiles loaded ahead of the one scored
+  static_assert(NS * T::kBytes <= 65536 && NS * T::vBytes <= 65536,
+                "each LDS region within one 16-bit read offset");
   __shared__ __attribute__((aligned(1024))) char smem[NS * T::bytes];
+  // K half and V^T half of LDS slot s
+  auto kb = [&](int s) { return smem + s * T::kBytes; };
+  auto vb = [&](int s) { return smem + NS * T::kBytes + s * T::vBytes; };
   __shared__ int32_t pg_lds[kMaxSplitPages];   // page ids of the full tiles
 
   int wg = blockIdx.x;
@@ -225,28 +255,39 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   const int hf = lane >> 5;         // which half of the k slots
   const int rows = a.W * a.G;
 
-  // ---- register-staged loads.  A tile is four 4 KB blocks (D = 128; 2 KB
-  // for D = 64): the K rows of page 0 and page 1, then the V^T rows of page
-  // 0 and page 1, each contiguous in the cache.  Chunk g = wave*64*CPT +
+  // ---- tile loads.  A tile is four 4 KB blocks (D = 128; 2 KB for
+  // D = 64): the K rows of page 0 and page 1, then the V^T rows of page 0
+  // and page 1, each contiguous in the cache.  Chunk g = wave*64*CPT +
   // u*64 + lane (16 bytes) belongs to block g / BC, so the block of a
   // (wave, u) pair is wave-uniform: every load is a raw buffer load through
-  // a per-page resource (scalar registers) at a fixed per-lane offset, and
-  // lands at a fixed per-lane LDS offset.
+  // a per-page resource (scalar registers) at a fixed per-lane offset.
+  // Full prefix tiles go straight to LDS: one load instruction fills 1 KB
+  // of its slot in lane order, so the swizzle is applied on the HBM side
+  // (lane l fetches the chunk whose swizzled home is byte 16*l of that
+  // kilobyte).  The boundary tiles go through registers (g_voff: chunk
+  // order in HBM, l_off: its swizzled LDS home).
   constexpr int NT = NW * kWave;
   constexpr int BC = kPage * D / 8;          // 16-byte chunks per block
   constexpr int CPT = 4 * BC / NT;           // chunks per thread per tile
   static_assert(4 * BC % NT == 0 && (64 * CPT) % 64 == 0, "chunk split");
-  int g_voff[CPT], l_off[CPT], g_blk[CPT];
+  int g_voff[CPT], l_off[CPT], g_blk[CPT], d_voff[CPT];
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
 #pragma unroll
   for (int u = 0; u < CPT; ++u) {
     const int g = wave * 64 * CPT + u * 64 + lane;
     const int blk = g / BC, c = g % BC;
     g_blk[u] = __builtin_amdgcn_readfirstlane(blk);
     g_voff[u] = c * 16;
+    // c is also the 16-byte position within the block in LDS order
     if (blk < 2) {
       l_off[u] = T::k_off(blk * kPage + c / (D / 8), c % (D / 8));
+      const int kip = c / (D / 8), slot = c % (D / 8);
+      d_voff[u] = kip * 2 * D +
+                  ((slot ^ T::swz_k(blk * kPage + kip)) << 4);
     } else {
       l_off[u] = T::v_off(blk - 2, c / 2, c % 2);
+      const int d = c / 2, slot = c % 2;
+      d_voff[u] = d * 32 + ((slot ^ ((d >> 3) & 1)) << 4);
     }
   }
   const int32_t* btb = a.bt + static_cast<int64_t>(b) * a.max_pages;
@@ -258,8 +299,9 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   auto ids_of = [&](int t) {
     return *reinterpret_cast<const int2*>(pg_lds + 2 * t);
   };
-  // global loads of a full prefix tile into a register stage
-  auto fetch_ids = [&](int2 ids, u16x8_t (&r)[CPT]) {
+  // a full prefix tile straight into LDS slot s: wave chunk g = wave*CPT +
+  // u is kilobyte g of the slot's K half (g < 2 blocks) or of its V^T half
+  auto dma_ids = [&](int2 ids, int s) {
     const int pg[2] = {__builtin_amdgcn_readfirstlane(ids.x),
                        __builtin_amdgcn_readfirstlane(ids.y)};
 #pragma unroll
@@ -269,17 +311,20 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
       const uint16_t* base = ((blk < 2) ? a.kc : a.vc) +
                              (static_cast<int64_t>(h ? pg[1] : pg[0]) * a.Hkv + kvh) *
                                  kPage * D;
-      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<uint16_t*>(base), 0, kBlockBytes, kBufferFlags);
-      r[u] = __builtin_bit_cast(
-          u16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, g_voff[u], 0, 0));
+      constexpr int kChunks = T::kBytes / 1024;
+      const int g = wave_u * CPT + u;
+      char* dp = (blk < 2) ? kb(s) + g * 1024 : vb(s) + (g - kChunks) * 1024;
+      const uint32_t dst =
+          static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)dp));
+      load_to_lds16(buffer_rsrc(base, kBlockBytes), d_voff[u],
+                    __builtin_amdgcn_readfirstlane(dst));
     }
   };
-  auto fetch = [&](int t, u16x8_t (&r)[CPT]) { fetch_ids(ids_of(t), r); };
-  auto stash = [&](const u16x8_t (&r)[CPT], char* sb) {
+  auto stash = [&](const u16x8_t (&r)[CPT], int s) {
 #pragma unroll
     for (int u = 0; u < CPT; ++u)
-      *reinterpret_cast<u16x8_t*>(sb + l_off[u]) = r[u];
+      *reinterpret_cast<u16x8_t*>((g_blk[u] < 2 ? kb(s) : vb(s)) + l_off[u]) =
+          r[u];
   };
 
   // ---- queries (B operand of S^T = K . Q^T)
@@ -325,7 +370,8 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   // ---- the three phases of one tile
   const int krow = key_of_row(col);
   // S^T for this wave's query columns from the K tile at stage sb
-  auto qk = [&](const char* sb, floatx16_t (&sc)[QB]) {
+  auto qk = [&](int slot, floatx16_t (&sc)[QB]) {
+    const char* sb = kb(slot);
 #pragma unroll
     for (int q = 0; q < QB; ++q)
 #pragma unroll
@@ -415,15 +461,19 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
     softmax_max(sc, need_mask, base, lim_pre, is_win, mc);
     softmax_exp(sc, mc, pf);
   };
-  // V^T fragments of a tile: the A operands of the P.V MFMAs
-  auto vread = [&](const char* sb, bf16x8_t (&vf)[2][NM]) {
+  // V^T fragments of a tile: the A operands of the P.V MFMAs.  Row
+  // m*32 + col keeps the swizzle bit of row col, so every fragment is this
+  // lane's offset plus a constant (folded into the read's offset field).
+  const int v_lane = T::v_off(0, col, hf);
+  auto vread = [&](int slot, bf16x8_t (&vf)[2][NM]) {
+    const char* sb = vb(slot) + v_lane;
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
       for (int m = 0; m < NM; ++m)
         vf[h2][m] = __builtin_bit_cast(
             bf16x8_t, *reinterpret_cast<const u16x8_t*>(
-                          sb + T::v_off(h2, m * 32 + col, hf)));
+                          sb + h2 * D * 32 + m * 32 * 32));
   };
   // O^T += V^T . P^T
   auto pv = [&](const bf16x8_t (&vf)[2][NM], const bf16x8_t (&pf)[QB][2]) {
@@ -437,23 +487,26 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
                                                             o[q][m], 0, 0, 0);
   };
 
-  // ---- full prefix tiles.  Tile t lives in LDS slot t % 6; tiles
-  // t+4 .. t+3+PF are in flight in PF register stages.  Iteration t runs
-  // the score MFMAs of tile t+1, the softmax of tile t (VALU, under those
-  // MFMAs) and its P.V MFMAs, then moves tile t+3 from registers to LDS
-  // and refills that register stage with tile t+3+PF.  The workgroup
-  // synchronises after odd iterations only: a tile is written three
-  // iterations before its first read, so a barrier always lies between;
-  // a slot is rewritten only after two or more iterations that end in a
-  // barrier; and no slot being written is read in the same window.
+  // ---- full prefix tiles.  Tile t lives in LDS slot t % NS and is loaded
+  // LEAD iterations before the one that scores it.  Iteration t runs the
+  // softmax of tile t (VALU) under the score MFMAs of tile t+1, then the
+  // P.V MFMAs of tile t, and issues the loads of tile t+LEAD.  The K
+  // fragments run one step ahead: those of tile t+2 are read as soon as
+  // the score MFMAs of tile t+1 have taken theirs, so the next iteration's
+  // score MFMAs never wait on LDS; the V fragments of tile t are read at
+  // the top of iteration t, a whole softmax ahead of the P.V MFMAs that use
+  // them.  The workgroup synchronises after odd iterations
+  // only, each wave first waiting for its own loads of every tile up to
+  // t+4 (the tiles read before the next barrier).  A slot is reloaded only
+  // after a barrier that follows the last read of its previous tile
+  // (NS = LEAD + 2), and no slot being loaded is read in the same
+  // iteration.
   const bool partial_last = n_pre > 0 && (k1 - k0) % kTileKeys != 0;
   const int n_full = n_pre - (partial_last ? 1 : 0);
-  u16x8_t rs[PF][CPT];
   floatx16_t sbuf[2][QB];     // scores of tile t in sbuf[t & 1]
-  // Fetches and stashes are unconditional (indices past the last full tile
-  // re-read that tile; the surplus stashes land in a stage nobody reads),
-  // so the loads form one straight-line stream and every wait before a
-  // stash lets the younger tiles stay in flight.
+  // Loads are unconditional (indices past the last full tile re-read that
+  // tile into a slot nobody reads), so every wave issues the same number
+  // of loads per iteration and the waits before the barriers are static.
   const int last_full = n_full - 1;
   // page ids of the full tiles into LDS; an invalid id is clamped to page 0
   // (in bounds) and reported
@@ -466,35 +519,41 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
     pg_lds[i] = id;
   }
   __syncthreads();
+  constexpr int kInFlight = CPT * (LEAD - 4);   // loads younger than t+4
+  static_assert(LEAD >= 4, "publish horizon");
+  // K fragments of the next tile to score (read one step ahead)
+  bf16x8_t kf[NK];
+  auto kread = [&](int slot) {
+    const char* sb = kb(slot);
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk)
+      kf[kk] = __builtin_bit_cast(
+          bf16x8_t,
+          *reinterpret_cast<const u16x8_t*>(sb + T::k_off(krow, 2 * kk + hf)));
+  };
   if (n_full > 0) {
 #pragma unroll
-    for (int j = 0; j < PF; ++j) fetch(min(j, last_full), rs[j]);
-#pragma unroll
-    for (int j = 0; j < 3; ++j) {
-      stash(rs[j % PF], smem + j * T::bytes);
-      fetch(min(j + PF, last_full), rs[j % PF]);
-    }
+    for (int j = 0; j < LEAD; ++j)
+      dma_ids(ids_of(min(j, last_full)), j);
+    wait_vmcnt<kInFlight>();
     __syncthreads();
-    qk(smem, sbuf[0]);
+    qk(0, sbuf[0]);
+    kread(1);
   }
-  // page ids of the next fetch, read one iteration ahead of their use
-  int2 nid = ids_of(min(3 + PF, max(last_full, 0)));
+  // page ids of the next load, read one iteration ahead of their use
+  int2 nid = ids_of(min(LEAD, max(last_full, 0)));
   // Iteration t (j = t mod U, a compile-time constant after unrolling, so
-  // register stages, LDS slots and score buffers are static).  The body is
-  // one macro used twice below; written as a lambda instead, the compiler
-  // allocates registers differently and spills inside the main loop.
+  // LDS slots and score buffers are static).  The body is one macro used
+  // twice below; written as a lambda instead, the compiler allocates
+  // registers differently and spills inside the main loop.
 #define WEDLM_TILE_ITER                                                   \
-    /* K fragments of tile t+1 (past the last full tile the stage holds a  */\
-    /* re-read tile; that score block is never used)                       */\
-    const char* sk = smem + ((j + 1) % NS) * T::bytes;                    \
-    bf16x8_t kf[NK];                                                      \
-    _Pragma("unroll")                                                     \
-    for (int kk = 0; kk < NK; ++kk)                                       \
-      kf[kk] = __builtin_bit_cast(                                        \
-          bf16x8_t,                                                       \
-          *reinterpret_cast<const u16x8_t*>(sk + T::k_off(krow, 2 * kk + hf)));\
     bf16x8_t vf[2][NM];                                                   \
-    vread(smem + (j % NS) * T::bytes, vf);                                \
+    vread(j % NS, vf);                                                    \
+    {                                                                     \
+      const int2 cur = nid;                                               \
+      nid = ids_of(min(t + LEAD + 1, last_full));                         \
+      dma_ids(cur, (j + LEAD) % NS);                                      \
+    }                                                                     \
     float mc[QB];                                                         \
     softmax_max(sbuf[j & 1], false, 0, 0, false, mc);                     \
     /* one scheduling region: the score MFMAs of tile t+1 interleaved with */\
@@ -515,17 +574,16 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   /* one MFMA  */\
       __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   /* six VALU  */\
     }                                                                     \
+    /* K fragments of tile t+2 (a re-read tile past the last full one) */ \
+    kread((j + 2) % NS);                                                  \
     pv(vf, pf);                                                           \
-    stash(rs[(j + 3) % PF], smem + ((j + 3) % NS) * T::bytes);            \
-    {                                                                     \
-      const int2 cur = nid;                                               \
-      nid = ids_of(min(t + 4 + PF, last_full));                           \
-      fetch_ids(cur, rs[(j + 3) % PF]);                                   \
-    }                                                                     \
-    if (j & 1) __syncthreads();
+    if (j & 1) {                                                          \
+      __builtin_amdgcn_sched_barrier(0);                                  \
+      wait_vmcnt<kInFlight>();                                            \
+      __syncthreads();                                                    \
+    }
   {
-  constexpr int U = PF * NS / gcd_c(PF, NS);
-  static_assert(U % 2 == 0, "iteration parity must be static");
+  constexpr int U = NS % 2 == 0 ? NS : 2 * NS;
   // whole groups of U tiles with no exit inside, so the loop carries the
   // same in-flight loads around its back edge as it receives on entry and
   // the compiler's waits stay partial; then the remaining tiles
@@ -558,7 +616,7 @@ tiles_done:
   const int n_tail = (partial_last ? 1 : 0) + n_win;
   for (int tt = 0; tt < n_tail; ++tt) {
     const bool is_win = !(partial_last && tt == 0);
-    char* sb = smem + ((n_full + tt) % NS) * T::bytes;
+    const int ts = (n_full + tt) % NS;
     int base, lim = 0;
     if (!is_win) {
       base = k0 + n_full * kTileKeys;
@@ -597,7 +655,7 @@ tiles_done:
         r[u] = v;
       }
       __syncthreads();   // every wave is done with the stage being reused
-      stash(r, sb);
+      stash(r, ts);
     } else {
       base = (tt - (partial_last ? 1 : 0)) * kTileKeys;
       __syncthreads();
@@ -614,21 +672,21 @@ tiles_done:
               ((static_cast<int64_t>(b) * a.W + base + key) * a.Hkv + kvh) * D +
               cc * 8);
         if (!isv) {
-          *reinterpret_cast<u16x8_t*>(sb + T::k_off(key, cc)) = v;
+          *reinterpret_cast<u16x8_t*>(kb(ts) + T::k_off(key, cc)) = v;
         } else {
           const int h = key / kPage, kk = key % kPage;
 #pragma unroll
           for (int e = 0; e < 8; ++e)
-            *reinterpret_cast<uint16_t*>(sb + T::v_off(h, cc * 8 + e, kk / 8) +
+            *reinterpret_cast<uint16_t*>(vb(ts) + T::v_off(h, cc * 8 + e, kk / 8) +
                                          (kk % 8) * 2) = v[e];
         }
       }
     }
     __syncthreads();
-    qk(sb, sbuf[0]);
+    qk(ts, sbuf[0]);
     bf16x8_t pf[QB][2], vf[2][NM];
     softmax(sbuf[0], true, base, lim, is_win, pf);
-    vread(sb, vf);
+    vread(ts, vf);
     pv(vf, pf);
   }
 
@@ -754,19 +812,19 @@ int launch(const AttnArgs& a, const Plan& p, hipStream_t st) {
   const int grid = a.nsplit * a.B * a.Hkv * a.qblocks;
   switch (p.sh.nw) {
     case 8:
-      hipLaunchKernelGGL((window_attn_kernel<D, 8, 1, 3>), dim3(grid),
+      hipLaunchKernelGGL((window_attn_kernel<D, 8, 1>), dim3(grid),
                          dim3(8 * kWave), 0, st, a);
       break;
     case 4:
-      hipLaunchKernelGGL((window_attn_kernel<D, 4, 1, 3>), dim3(grid),
+      hipLaunchKernelGGL((window_attn_kernel<D, 4, 1>), dim3(grid),
                          dim3(4 * kWave), 0, st, a);
       break;
     case 2:
-      hipLaunchKernelGGL((window_attn_kernel<D, 2, 1, 2>), dim3(grid),
+      hipLaunchKernelGGL((window_attn_kernel<D, 2, 1>), dim3(grid),
                          dim3(2 * kWave), 0, st, a);
       break;
     default:
-      hipLaunchKernelGGL((window_attn_kernel<D, 1, 1, 2>), dim3(grid),
+      hipLaunchKernelGGL((window_attn_kernel<D, 1, 1>), dim3(grid),
                          dim3(kWave), 0, st, a);
       break;
   }
