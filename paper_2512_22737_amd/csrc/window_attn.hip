@@ -301,6 +301,11 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   };
   // a full prefix tile straight into LDS slot s: wave chunk g = wave*CPT +
   // u is kilobyte g of the slot's K half (g < 2 blocks) or of its V^T half
+  // LDS byte address of smem: the loads' destinations are 32-bit LDS
+  // offsets computed in scalar registers
+  const uint32_t lds0 =
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)smem));
+  constexpr int kChunks = T::kBytes / 1024;
   auto dma_ids = [&](int2 ids, int s) {
     const int pg[2] = {__builtin_amdgcn_readfirstlane(ids.x),
                        __builtin_amdgcn_readfirstlane(ids.y)};
@@ -311,11 +316,11 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
       const uint16_t* base = ((blk < 2) ? a.kc : a.vc) +
                              (static_cast<int64_t>(h ? pg[1] : pg[0]) * a.Hkv + kvh) *
                                  kPage * D;
-      constexpr int kChunks = T::kBytes / 1024;
       const int g = wave_u * CPT + u;
-      char* dp = (blk < 2) ? kb(s) + g * 1024 : vb(s) + (g - kChunks) * 1024;
       const uint32_t dst =
-          static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)dp));
+          lds0 + ((blk < 2) ? s * T::kBytes + g * 1024
+                            : NS * T::kBytes + s * T::vBytes +
+                                  (g - kChunks) * 1024);
       load_to_lds16(buffer_rsrc(base, kBlockBytes), d_voff[u],
                     __builtin_amdgcn_readfirstlane(dst));
     }

@@ -74,6 +74,21 @@ def test_small_shapes(name, W, Hq, Hkv, D, pr, fr, V):
     _full_check(wl, WL.step_inputs(wl, seed=0))
 
 
+def test_eight_wave_tile_counts():
+    """256 query rows per kv head at D = 128 (eight waves, two per SIMD):
+    every count of full 32-key prefix tiles from 0 to 10 in one split,
+    with and without a partial last tile, so that both wave halves' barrier
+    schedules and the loop's remainder path meet every case."""
+    wl = WL.Workload("w64_g4_tiles", 70, B=14, W=64, Hq=8, Hkv=2, D=128,
+                     V=600, prefix=330, prefix_hi=330, obs_frac=0.0,
+                     obs_frac_hi=0.75, spike=9.0, spike_prob=0.5)
+    d = WL.step_inputs(wl, seed=0)
+    # the block tables cover 330 + W positions; shorter prefixes use a part
+    d["win_start"][:] = [0, 31, 32, 64, 95, 96, 128, 161, 192, 224, 256,
+                         288, 320, 330]
+    _full_check(wl, d)
+
+
 def test_all_masks_and_all_filled():
     wl = WL.Workload("edge", 60, B=4, W=16, Hq=4, Hkv=2, D=64, V=300,
                      prefix=0, prefix_hi=50, obs_frac=0.0, spike=9.0)
