@@ -89,6 +89,20 @@ def test_eight_wave_tile_counts():
     _full_check(wl, d)
 
 
+def test_prefix_beyond_one_split_of_pages():
+    """A prefix longer than one split's staged page ids (2048 pages, 32,768
+    positions) on a grid that already fills the CUs (16 sequences x 16 kv
+    heads = 256 workgroups): the plan must still split it (two splits of
+    516 tiles) and merge them.  Attention checked on sampled sequences,
+    rows and heads."""
+    wl = WL.Workload("split_pages", 71, B=16, W=16, Hq=16, Hkv=16, D=64,
+                     V=500, prefix=33000, prefix_hi=33000, obs_frac=0.0,
+                     obs_frac_hi=0.75, spike=9.0, spike_prob=0.5)
+    d = WL.step_inputs(wl, seed=0)
+    _full_check(wl, d, [0, 9, 15], lambda b, n: _sample_rows(b, n, wl.W),
+                lambda b: sorted({0, 6, 15, (3 * b) % 16}))
+
+
 def test_all_masks_and_all_filled():
     wl = WL.Workload("edge", 60, B=4, W=16, Hq=4, Hkv=2, D=64, V=300,
                      prefix=0, prefix_hi=50, obs_frac=0.0, spike=9.0)
