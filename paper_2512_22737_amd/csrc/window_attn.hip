@@ -75,6 +75,7 @@ Shape pick_shape(int rows) {
 
 struct Plan {
   Shape sh;
+  bool two;               // four-wave workgroups, two per CU
   int rows, rows_per_wg, qblocks, rows_pad, nsplit, split_len;
   size_t ws_bytes;
 };
@@ -89,7 +90,10 @@ Plan make_plan(int B, int W, int Hq, int Hkv, int D, int max_prefix) {
   p.rows_pad = p.qblocks * p.rows_per_wg;
   const int tiles = (max_prefix + kTileKeys - 1) / kTileKeys;
   const int base = B * Hkv * p.qblocks;
-  const int target = 256;   // one workgroup per CU
+  // one workgroup per CU; four-wave workgroups run two per CU when the
+  // grid has 512 without splitting (more splits cost more than they gain)
+  p.two = p.sh.nw == 4 && base >= 512;
+  const int target = 256;
   int nsplit = (target + base - 1) / base;
   const int max_split = tiles / 8 > 1 ? tiles / 8 : 1;  // >= 8 tiles each
   if (nsplit > max_split) nsplit = max_split;
@@ -212,13 +216,25 @@ __device__ __forceinline__ int key_of_row(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
 
-template <int D, int NW, int QB>
-__global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
+// TWO: four-wave workgroups (128 query rows per kv head) that run two per
+// CU, so that every SIMD holds two waves, on grids of at least 512
+// workgroups: their ring is four slots (64 KB at D = 128), small enough for
+// two workgroups' LDS, with a barrier after every tile.  Otherwise one
+// workgroup per CU with an eight-slot ring, a barrier every two tiles and
+// the K fragments read one step ahead.
+template <int D, int NW, int QB, bool TWO>
+__global__ __launch_bounds__(NW * kWave)
+__attribute__((amdgpu_waves_per_eu(TWO ? 2 : 1)))
+void window_attn_kernel(AttnArgs a) {
   using T = Tile<D>;
   constexpr int NK = D / 16;          // k-steps of the score MFMA
   constexpr int NM = D / 32;          // 32-row blocks of O^T
-  constexpr int NS = 8;               // LDS ring of 32-key tile slots
-  constexpr int LEAD = NS - 2;        // tiles loaded ahead of the one scored
+  static_assert(!TWO || NW == 4, "two per CU: four-wave workgroups");
+  constexpr bool kTwo = TWO;
+  constexpr bool kHoist = !kTwo;      // K fragments read one step ahead
+  constexpr int kBarEvery = kTwo ? 1 : 2;   // iterations per barrier
+  constexpr int NS = kTwo ? 4 : 8;    // LDS ring of 32-key tile slots
+  constexpr int LEAD = kTwo ? 3 : NS - 2;   // tiles loaded ahead of the one scored
   static_assert(NS * T::kBytes <= 65536 && NS * T::vBytes <= 65536,
                 "each LDS region within one 16-bit read offset");
   __shared__ __attribute__((aligned(1024))) char smem[NS * T::bytes];
@@ -524,9 +540,14 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
     pg_lds[i] = id;
   }
   __syncthreads();
-  constexpr int kInFlight = CPT * (LEAD - 4);   // loads younger than t+4
-  static_assert(LEAD >= 4, "publish horizon");
-  // K fragments of the next tile to score (read one step ahead)
+  // Tiles published at a barrier: with the K fragments one step ahead and
+  // a barrier every two iterations, every tile up to t+4; without them and
+  // a barrier every iteration, every tile up to t+2.
+  constexpr int kHorizon = kHoist ? 4 : 2;
+  constexpr int kInFlight = CPT * (LEAD - kHorizon);   // younger loads
+  static_assert(LEAD > kHorizon, "publish horizon");
+  static_assert(kHoist ? NS >= LEAD + 2 : NS >= LEAD + 1, "slot reuse");
+  // K fragments of the next tile to score
   bf16x8_t kf[NK];
   auto kread = [&](int slot) {
     const char* sb = kb(slot);
@@ -543,7 +564,7 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
     wait_vmcnt<kInFlight>();
     __syncthreads();
     qk(0, sbuf[0]);
-    kread(1);
+    if constexpr (kHoist) kread(1);
   }
   // page ids of the next load, read one iteration ahead of their use
   int2 nid = ids_of(min(LEAD, max(last_full, 0)));
@@ -552,6 +573,7 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
   // twice below; written as a lambda instead, the compiler allocates
   // registers differently and spills inside the main loop.
 #define WEDLM_TILE_ITER                                                   \
+    if constexpr (!kHoist) kread((j + 1) % NS);                           \
     bf16x8_t vf[2][NM];                                                   \
     vread(j % NS, vf);                                                    \
     {                                                                     \
@@ -580,15 +602,15 @@ __global__ __launch_bounds__(NW * kWave) void window_attn_kernel(AttnArgs a) {
       __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   /* six VALU  */\
     }                                                                     \
     /* K fragments of tile t+2 (a re-read tile past the last full one) */ \
-    kread((j + 2) % NS);                                                  \
+    if constexpr (kHoist) kread((j + 2) % NS);                            \
     pv(vf, pf);                                                           \
-    if (j & 1) {                                                          \
+    if ((j % kBarEvery) == kBarEvery - 1) {                               \
       __builtin_amdgcn_sched_barrier(0);                                  \
       wait_vmcnt<kInFlight>();                                            \
       __syncthreads();                                                    \
     }
   {
-  constexpr int U = NS % 2 == 0 ? NS : 2 * NS;
+  constexpr int U = NS % kBarEvery == 0 ? NS : kBarEvery * NS;
   // whole groups of U tiles with no exit inside, so the loop carries the
   // same in-flight loads around its back edge as it receives on entry and
   // the compiler's waits stay partial; then the remaining tiles
@@ -817,19 +839,23 @@ int launch(const AttnArgs& a, const Plan& p, hipStream_t st) {
   const int grid = a.nsplit * a.B * a.Hkv * a.qblocks;
   switch (p.sh.nw) {
     case 8:
-      hipLaunchKernelGGL((window_attn_kernel<D, 8, 1>), dim3(grid),
+      hipLaunchKernelGGL((window_attn_kernel<D, 8, 1, false>), dim3(grid),
                          dim3(8 * kWave), 0, st, a);
       break;
     case 4:
-      hipLaunchKernelGGL((window_attn_kernel<D, 4, 1>), dim3(grid),
-                         dim3(4 * kWave), 0, st, a);
+      if (p.two)
+        hipLaunchKernelGGL((window_attn_kernel<D, 4, 1, true>), dim3(grid),
+                           dim3(4 * kWave), 0, st, a);
+      else
+        hipLaunchKernelGGL((window_attn_kernel<D, 4, 1, false>), dim3(grid),
+                           dim3(4 * kWave), 0, st, a);
       break;
     case 2:
-      hipLaunchKernelGGL((window_attn_kernel<D, 2, 1>), dim3(grid),
+      hipLaunchKernelGGL((window_attn_kernel<D, 2, 1, false>), dim3(grid),
                          dim3(2 * kWave), 0, st, a);
       break;
     default:
-      hipLaunchKernelGGL((window_attn_kernel<D, 1, 1>), dim3(grid),
+      hipLaunchKernelGGL((window_attn_kernel<D, 1, 1, false>), dim3(grid),
                          dim3(kWave), 0, st, a);
       break;
   }

@@ -89,6 +89,21 @@ def test_eight_wave_tile_counts():
     _full_check(wl, d)
 
 
+def test_four_wave_two_per_cu_tile_counts():
+    """128 query rows per kv head on a grid of 512 workgroups (64 sequences
+    x 8 kv heads): the four-wave kernel that runs two workgroups per CU,
+    with its four-slot ring and a barrier after every tile.  Prefixes give
+    every count of full tiles from 0 to 10, with and without a partial
+    tile; attention checked on those sequences."""
+    wl = WL.Workload("w16_g8_two", 72, B=64, W=16, Hq=64, Hkv=8, D=64,
+                     V=300, prefix=330, prefix_hi=330, obs_frac=0.0,
+                     obs_frac_hi=0.75, spike=9.0, spike_prob=0.5)
+    d = WL.step_inputs(wl, seed=0)
+    lens = [0, 31, 32, 64, 95, 96, 128, 161, 192, 224, 256, 288, 320, 330]
+    d["win_start"][:len(lens)] = lens
+    _full_check(wl, d, list(range(len(lens))) + [40, 63])
+
+
 def test_prefix_beyond_one_split_of_pages():
     """A prefix longer than one split's staged page ids (2048 pages, 32,768
     positions) on a grid that already fills the CUs (16 sequences x 16 kv
