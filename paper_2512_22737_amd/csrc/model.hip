@@ -441,7 +441,7 @@ struct Gemm2dArgs {
   const uint16_t* x;      // packed activations, ceil(M/32) row tiles
   const uint16_t* w;      // packed weights
   void* out;
-  float* part;            // n_ks > 1 (residual add): [n_ks, M, N]
+  float* part;            // n_ks > 1 (residual add, stored q|k|v): [n_ks, M, N]
   int M, N, K, ldo;
   int n_fb;               // 32-feature blocks of the output (N / 32)
   int n_ft, n_tt, n_ks;   // feature tiles, row tiles, K splits
@@ -579,12 +579,12 @@ __global__ __launch_bounds__(kGThreads) void gemm2d_kernel(Gemm2dArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) v[r] = acc[fi][tj][4 * g + r];
           const int64_t o = static_cast<int64_t>(tok) * a.ldo + f;
-          if constexpr (EPI == kStoreBf16) {
+          if (EPI == kStoreBf16 && a.n_ks == 1) {
             u16x4_t h;
 #pragma unroll
             for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(v[r]);
             *reinterpret_cast<u16x4_t*>(static_cast<uint16_t*>(a.out) + o) = h;
-          } else if (a.n_ks == 1) {
+          } else if (EPI == kAddF32 && a.n_ks == 1) {
             floatx4_t* p = reinterpret_cast<floatx4_t*>(static_cast<float*>(a.out) + o);
             const floatx4_t old = *p;
 #pragma unroll
@@ -598,6 +598,29 @@ __global__ __launch_bounds__(kGThreads) void gemm2d_kernel(Gemm2dArgs a) {
       }
     }
   }
+}
+
+// out[t][n] (bf16) = sum over splits k (in order) of part[k][t][n], four
+// consecutive n per thread (N a multiple of 32, ldo of 4)
+__global__ __launch_bounds__(256) void sum_partials_bf16_kernel(
+    uint16_t* __restrict__ out, int ldo, const float* __restrict__ part,
+    int n_ks, int M, int N) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t n4 = N / 4;
+  if (i >= static_cast<int64_t>(M) * n4) return;
+  const int64_t t = i / n4;
+  const int n = static_cast<int>(i % n4) * 4;
+  floatx4_t v = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < n_ks; ++k) {
+    const floatx4_t p = *reinterpret_cast<const floatx4_t*>(
+        part + (static_cast<int64_t>(k) * M + t) * N + n);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] += p[r];
+  }
+  u16x4_t h;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(v[r]);
+  *reinterpret_cast<u16x4_t*>(out + t * ldo + n) = h;
 }
 
 // rows past M in the last tile are zero: a row-major activation matrix
@@ -706,7 +729,9 @@ GemmPlan gemm_plan(int M, int N, int K, int epi, bool xp = false) {
     p.n_ft = (p.n_nb + (epi == kSwiglu ? 3 : 7)) / (epi == kSwiglu ? 4 : 8);
     p.n_tt = (M + 32 * k2dTok - 1) / (32 * k2dTok);
     p.n_ks = 1;
-    if (epi == kAddF32)
+    // a stored product (q|k|v) with few tiles splits K too; its fp32
+    // partials are summed into bf16 right after
+    if (epi == kAddF32 || epi == kStoreBf16)
       p.n_ks = std::max(1, std::min(kGemmTargetWgs / (p.n_ft * p.n_tt),
                                     K / kKStep / 4));
     if (p.n_ks > 1)
@@ -757,7 +782,13 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
                          dim3(kGThreads), 0, st, g);
     WEDLM_LAUNCH_CHECK();
     if (n_ks_out) *n_ks_out = p.n_ks;
-    if (p.n_ks > 1 && !defer) {
+    if (p.n_ks > 1 && epi == kStoreBf16) {
+      const int64_t total4 = static_cast<int64_t>(M) * (N / 4);
+      hipLaunchKernelGGL(sum_partials_bf16_kernel, dim3((total4 + 255) / 256),
+                         dim3(256), 0, st, static_cast<uint16_t*>(out), ldo,
+                         g.part, p.n_ks, M, N);
+      WEDLM_LAUNCH_CHECK();
+    } else if (p.n_ks > 1 && !defer) {
       const int64_t total = static_cast<int64_t>(M) * N;
       hipLaunchKernelGGL(add_partials_kernel, dim3((total + 255) / 256),
                          dim3(256), 0, st, static_cast<float*>(out), ldo,
@@ -839,10 +870,13 @@ Carve carve(const wedlm_model_config* c, int B, int W, int max_prefix_len) {
   // next RMSNorm before the other is written)
   const int Mi = static_cast<int>(M);
   const bool big = Mi >= k2dMinRows;   // o's input packed (2-D kernel)
+  // and of the q|k|v product (summed right after it)
   k.part_bytes = std::max(
-      gemm_plan(Mi, c->hidden, c->n_heads * c->head_dim, kAddF32, big)
-          .part_bytes,
-      gemm_plan(Mi, c->hidden, c->inter, kAddF32, true).part_bytes);
+      std::max(gemm_plan(Mi, c->hidden, c->n_heads * c->head_dim, kAddF32, big)
+                   .part_bytes,
+               gemm_plan(Mi, c->hidden, c->inter, kAddF32, true).part_bytes),
+      gemm_plan(Mi, (c->n_heads + 2 * c->n_kv_heads) * c->head_dim, c->hidden,
+                kStoreBf16, true).part_bytes);
   k.part = off; off += up256(k.part_bytes);
   k.x = off;    off += up256(M * Hd * 4);
   const size_t Mp = (M + 31) / 32 * 32;           // packed: whole tiles
@@ -1020,7 +1054,7 @@ extern "C" int wedlm_model_forward(
                    wt->attn_norm + static_cast<int64_t>(l) * Hd, cfg->rms_eps,
                    xn, true, st));
     WEDLM_TRY(gemm(xn, wt->w_qkv + static_cast<int64_t>(l) * QKV * Hd, M, QKV,
-                   Hd, qkv, QKV, kStoreBf16, nullptr, 0, true, true, st));
+                   Hd, qkv, QKV, kStoreBf16, part, part_bytes, true, true, st));
     WEDLM_TRY(wedlm_qk_norm_rope(qkv, wt->q_norm + static_cast<int64_t>(l) * D,
                                  wt->k_norm + static_cast<int64_t>(l) * D,
                                  pos_ids, M, Hq, Hkv, D, cfg->rope_theta,
