@@ -7,12 +7,20 @@ are already resident in HBM.  Every step starts from the workload's own
 window state (a fresh device copy per step, made before the timed region),
 so every timed step does the configured workload's work.
 Small workloads rotate over several input sets so that no timed step finds
-its inputs in the 256 MB last-level cache.
+its inputs in the 256 MB last-level cache.  --graph replays each step from a
+HIP graph (the window reset inside it), which removes the host's launch
+gaps from the small workloads' steps.
 
 Prints ONE JSON line: window tokens/s (B*W per step time), the roofline of
 the dominant kernel (window attention: algorithmic bytes per launch over its
 HIP-event-timed average duration, against 8 TB/s), and the fp64 CPU oracle
 timed on a bounded sample of the same workload.
+
+--workload stream512 runs Algorithm 1's loop instead: all 512 steps of the
+streaming workload on one persistent window state and cache (the prefix
+grows as tokens commit), each step's inputs staged before it, HIP events
+around each call; the line reports the mean window tokens/s, algorithmic
+GB/s and p_cache (Eq. 4) over the loop.
 
 --lm-head instead times wedlm_lm_head_score (the output layer fused with
 the row score) at the Qwen3-8B output-layer shape (Hd 4096, V 151936) for
@@ -414,19 +422,180 @@ def compare_rules(args, dev):
                 "status_nonzero": st}), flush=True)
 
 
+def stream_loop(args, dev, wl):
+    """Config 5 as Algorithm 1's loop: every step of the streaming workload
+    (16 sequences from prefix 1024, W=32, all-mask start) on one persistent
+    window state and cache, so the prefix grows as tokens commit.  Each
+    step's inputs (seeded Q/K/V, cycled over 16 drawn sets since they enter
+    no decision, and that step's seeded logits, built on the device) are
+    staged before the step; HIP events around each of the four calls time
+    the step's kernels only.  Reports the mean over all steps: window
+    tokens/s, algorithmic bytes per second of step time, p_cache (Eq. 4),
+    and the attention and score kernels' own time per step."""
+    import numpy as np
+    import torch
+    from paper_2512_22737_amd import wedlm
+    from paper_2512_22737_amd import workloads as WL
+    S, seed = wl.steps, args.seed
+    print(f"# generating inputs for {wl.name}", file=sys.stderr, flush=True)
+    d = WL.step_inputs(wl, seed=seed)
+
+    def up(a):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        if a.dtype == np.uint16:
+            t = t.view(torch.int16).view(torch.bfloat16)
+        return t.to(dev)
+
+    st = {k: up(v) for k, v in d.items() if isinstance(v, np.ndarray)}
+    qkv_sets = [st["qkv_in"]] + [up(WL.qkv(wl, seed, t)) for t in range(1, 16)]
+    pool = torch.from_numpy(WL.logit_pool(wl, seed)).to(dev)
+    c0 = d["win_start"].copy()
+    step = wedlm.DecodeStep(wl.B, wl.W, wl.Hq, wl.Hkv, wl.D, wl.V,
+                            int(c0.max()) + S * wl.W, theta=wl.theta,
+                            tau=wl.tau, lam=wl.lam, temperature=wl.temp,
+                            device=dev)
+    init_tok, init_start = st["win_tok"].clone(), st["win_start"].clone()
+    # every step's logits row draws (pool row, cyclic shift, spike token,
+    # spiked or not), staged on the device before the loop so that building
+    # a step's logits needs no host-to-device copy (which would stall the
+    # host and open gaps between the step's launches)
+    n = wl.B * wl.W
+    prm = [WL.logit_row_params(wl, seed, t) for t in range(S)]
+    idx_d = torch.as_tensor(np.stack([p[0] for p in prm]), device=dev)
+    shift_d = torch.as_tensor(np.stack([p[1] for p in prm]), device=dev)
+    add_d = torch.as_tensor(np.stack([p[2] for p in prm]).astype(np.float32) *
+                            np.float32(wl.spike), device=dev)
+    tok_d = torch.as_tensor(np.stack([p[3] for p in prm]), device=dev)
+    ar = torch.arange(wl.V, device=dev, dtype=torch.int64)
+    rows_n = torch.arange(n, device=dev)
+
+    def make_logits(t):
+        # the rows of WL.logits_torch(wl, pool, seed, t): a cyclic shift of
+        # a pool row each, plus the spike on its token in spiked rows
+        col = (ar[None, :] - shift_d[t][:, None]) % wl.V
+        out = torch.gather(pool[idx_d[t]], 1, col)
+        out[rows_n, tok_d[t]] += add_d[t]
+        return out.view(wl.B, wl.W, wl.V)
+
+    def run(t, ev=None):
+        logits = make_logits(t)
+        calls = (
+            lambda: step.reorder(st["win_tok"], st["win_start"],
+                                 qkv_sets[t % 16]),
+            lambda: step.attn(st["k_cache"], st["v_cache"],
+                              st["block_table"], st["win_start"]),
+            lambda: step.score(logits),
+            lambda: step.commit(st["win_tok"], st["win_start"],
+                                st["k_cache"], st["v_cache"],
+                                st["block_table"]))
+        for i, call in enumerate(calls):
+            if ev is not None:
+                ev[i].record()
+            call()
+        if ev is not None:
+            ev[4].record()
+
+    # warmup steps from the initial state; the state is then restored (the
+    # cache rows they appended lie past every prefix and are rewritten when
+    # their positions commit again)
+    for t in range(args.warmup):
+        run(t)
+    torch.cuda.synchronize()
+    st["win_tok"].copy_(init_tok)
+    st["win_start"].copy_(init_start)
+    c_hist = torch.empty(S, wl.B, dtype=torch.int32, device=dev)
+    nobs_hist = torch.empty(S, wl.B, dtype=torch.int32, device=dev)
+    n_hist = torch.empty(S, wl.B, dtype=torch.int32, device=dev)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)]
+           for _ in range(S)]
+    torch.cuda.synchronize()
+    for t in range(S):
+        c_hist[t].copy_(st["win_start"])
+        run(t, evs[t])
+        nobs_hist[t].copy_(step.n_obs)
+        n_hist[t].copy_(step.n_commit)
+    torch.cuda.synchronize()
+    iv = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)]
+                   for e in evs]) * 1e3                    # us, [S, 4]
+    step_us = iv.sum(axis=1)
+    c_h = c_hist.cpu().numpy().astype(np.int64)
+    masked = (wl.W - nobs_hist.cpu().numpy()).astype(np.int64)
+    n_h = n_hist.cpu().numpy().astype(np.int64)
+    status = int(step.status.abs().sum().item() +
+                 step.attn_status.abs().sum().item())
+    if status:
+        print(f"# warning: nonzero status words ({status})", file=sys.stderr)
+    a_bytes = np.array([attn_bytes(wl, c_h[t]) for t in range(S)],
+                       dtype=np.float64)
+    s_bytes = np.array([step_bytes(wl, c_h[t], int(masked[t].sum()),
+                                   int(n_h[t].sum())) for t in range(S)],
+                       dtype=np.float64)
+    score_bytes = 4.0 * wl.V * masked.sum(axis=1)
+    tot_s = step_us.sum() * 1e-6
+    attn_s = iv[:, 1].sum() * 1e-6
+    score_s = iv[:, 2].sum() * 1e-6
+    achieved = a_bytes.sum() / attn_s / 1e9
+    res = {
+        "metric": METRIC,
+        "value": wl.B * wl.W * S / tot_s,
+        "unit": "window tokens/s",
+        "n_gpus": 1,
+        "steps": S,
+        "warmup": args.warmup,
+        "ms_per_step": step_us.mean() / 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B,
+                   "prefix_start": int(c0.min()),
+                   "prefix_end": int(c_h[-1].max() + n_h[-1].max()),
+                   "W": wl.W, "Hq": wl.Hq, "Hkv": wl.Hkv, "D": wl.D,
+                   "V": wl.V, "tau": wl.tau, "lambda": wl.lam,
+                   "temperature": wl.temp, "loop": "persistent state",
+                   "timing": "HIP events around each call of every step"},
+        "p_cache": float(n_h.sum()) / (S * wl.B * wl.W),
+        "committed_tokens": int(n_h.sum()),
+        "committed_tokens_per_s": float(n_h.sum()) / tot_s,
+        "roofline": {"kernel": "wedlm_window_attn", "bound": "hbm",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": None,
+                     "alg_bytes_per_launch": float(a_bytes.mean()),
+                     "avg_launch_us": iv[:, 1].mean()},
+        "score": {"avg_launch_us": iv[:, 2].mean(),
+                  "alg_bytes_per_launch": float(score_bytes.mean()),
+                  "achieved_gbps": score_bytes.sum() / score_s / 1e9},
+        "step_alg_bytes": float(s_bytes.mean()),
+        "step_hbm_gbps": s_bytes.sum() / tot_s / 1e9,
+        "step_frac": s_bytes.sum() / tot_s / 1e9 / HBM_PEAK_GBPS,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("# timing the oracle on a sample", file=sys.stderr, flush=True)
+        # step 0 of the loop (all-mask windows at the starting prefix)
+        d0 = dict(d, logits=WL.logits(wl, None, seed, 0,
+                                      pool=WL.logit_pool(wl, seed)))
+        res["cpu_baseline"] = cpu_baseline(wl, d0, seed)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    # The decode step's defaults (200 timed after 300 warmup steps) reach
-    # the clock's steady state under this load: after a few back-to-back
-    # steps the power controller first pulls the clock well below its
-    # sustained level and recovers over ~100 ms of load.  The other modes
-    # default to 20 timed after 5 warmup steps.
-    ap.add_argument("--steps", type=int, default=None)
-    ap.add_argument("--warmup", type=int, default=None)
+    # 20 timed steps after 5 warmup steps by default.  Under this load the
+    # power controller first pulls the clock well below its sustained level
+    # and recovers over ~100 ms of back-to-back steps; --steps 200 --warmup
+    # 300 measures the sustained clock instead.
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="long_prefix")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each step from a HIP graph (no host launch "
+                         "gaps; for the small single-step workloads)")
     ap.add_argument("--compare-rules", action="store_true",
                     help="p_cache and committed tokens/s of the decoding "
                          "rules on the streaming workload, then exit")
@@ -445,12 +614,6 @@ def main():
                     help="only run a plain device copy of this size (for "
                          "scaling HBM counters) and exit")
     args = ap.parse_args()
-    step_mode = not (args.compare_rules or args.lm_head or args.model or
-                     args.dual_stream or args.copy_calibration_mib)
-    if args.steps is None:
-        args.steps = 200 if step_mode else 20
-    if args.warmup is None:
-        args.warmup = 300 if step_mode else 5
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is "
               "not supported (the multi-GPU sharding is a design note only)",
@@ -491,7 +654,8 @@ def main():
 
     wl = WL.WORKLOADS[args.workload]
     if wl.steps > 1:
-        wl = wl.replace(steps=1)      # one step of the streaming shape
+        stream_loop(args, dev, wl)
+        return
     total_steps = args.warmup + args.steps
     print(f"# generating inputs for {wl.name}", file=sys.stderr, flush=True)
     d = WL.step_inputs(wl, seed=args.seed, nan_observed_rows=False)
@@ -531,30 +695,70 @@ def main():
         step.commit(win_tok, win_start, s["k_cache"], s["v_cache"],
                     s["block_table"])
 
-    # every step starts from the workload's own window: one fresh copy of
-    # the window state per step, made before the timed region (the commit
-    # rewrites the window and re-appends the same cache slots each step)
-    states = [(sets[t % n_sets]["win_tok"].clone(),
-               sets[t % n_sets]["win_start"].clone())
-              for t in range(total_steps)]
-
-    for t in range(args.warmup):
-        run(t)
-    torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True),
-            torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record()
-    for t in range(args.steps):
-        run(args.warmup + t, evs[t])
-    t_end.record()
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_step = total_ms / args.steps
-    attn_ms = [a.elapsed_time(b) for a, b in evs]
-    attn_avg_s = sum(attn_ms) / len(attn_ms) / 1e3
+    if args.graph:
+        # one HIP graph per input set: the set's window state reset from a
+        # stored copy (two small device copies), then the four calls; and
+        # one graph of the attention alone (on its own copy of the prefix
+        # lengths) for the kernel's launch time.  Replays go round the sets.
+        graphs, attn_graphs = [], []
+        for s in sets:
+            init = (s["win_tok"].clone(), s["win_start"].clone())
+            plen = s["win_start"].clone()
+            g, ga = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                s["win_tok"].copy_(init[0])
+                s["win_start"].copy_(init[1])
+                step.reorder(s["win_tok"], s["win_start"], s["qkv_in"])
+                step.attn(s["k_cache"], s["v_cache"], s["block_table"],
+                          s["win_start"])
+                step.score(s["logits"])
+                step.commit(s["win_tok"], s["win_start"], s["k_cache"],
+                            s["v_cache"], s["block_table"])
+            with torch.cuda.graph(ga):
+                step.attn(s["k_cache"], s["v_cache"], s["block_table"], plen)
+            graphs.append(g)
+            attn_graphs.append(ga)
+
+        def replay_loop(gs):
+            for t in range(args.warmup):
+                gs[t % n_sets].replay()
+            torch.cuda.synchronize()
+            t_start.record()
+            for t in range(args.steps):
+                gs[t % n_sets].replay()
+            t_end.record()
+            torch.cuda.synchronize()
+            return t_start.elapsed_time(t_end)
+
+        total_ms = replay_loop(graphs)
+        attn_avg_s = replay_loop(attn_graphs) / args.steps / 1e3
+        ms_step = total_ms / args.steps
+    else:
+        # every step starts from the workload's own window: one fresh copy
+        # of the window state per step, made before the timed region (the
+        # commit rewrites the window and re-appends the same cache slots)
+        states = [(sets[t % n_sets]["win_tok"].clone(),
+                   sets[t % n_sets]["win_start"].clone())
+                  for t in range(total_steps)]
+
+        for t in range(args.warmup):
+            run(t)
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True),
+                torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        t_start.record()
+        for t in range(args.steps):
+            run(args.warmup + t, evs[t])
+        t_end.record()
+        torch.cuda.synchronize()
+        total_ms = t_start.elapsed_time(t_end)
+        ms_step = total_ms / args.steps
+        attn_ms = [a.elapsed_time(b) for a, b in evs]
+        attn_avg_s = sum(attn_ms) / len(attn_ms) / 1e3
     status = int(step.status.abs().sum().item() +
                  step.attn_status.abs().sum().item())
     if status:
@@ -580,7 +784,8 @@ def main():
                    "prefix_min": int(c.min()), "W": wl.W, "Hq": wl.Hq,
                    "Hkv": wl.Hkv, "D": wl.D, "V": wl.V,
                    "masked_rows": n_masked, "tau": wl.tau, "lambda": wl.lam,
-                   "temperature": wl.temp, "input_sets": n_sets},
+                   "temperature": wl.temp, "input_sets": n_sets,
+                   "launch": "hip graph" if args.graph else "eager"},
         "roofline": {"kernel": "wedlm_window_attn", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,

@@ -20,8 +20,12 @@
 //   tile slots (buffer loads with the LDS-destination bit, no register
 //   staging), issued six tiles ahead; the workgroup synchronises once per
 //   two tiles.
-// Softmax: log2 domain, running max raised only when a tile's max exceeds
-//   it by more than 8 (p <= 2^8 otherwise), so the O rescale is rare.
+// Softmax: log2 domain, p = 2^(s*c - m) with c = softmax_scale * log2(e)
+//   folded into one FMA per score.  There is no per-tile max: m, a column's
+//   reference max, is the first tile's max and is raised only when the
+//   running sum shows that some term exceeded 2^64 (never for scores that
+//   grow by less than 64 log2 units past the first tile; a rare,
+//   wave-uniform branch otherwise).
 // Split-K: the prefix is split so that the grid fills the CUs; partials
 //   (unnormalised O, running max and sum) are merged by a combine kernel.
 //   With a single split the main kernel normalises and writes the output.
@@ -40,7 +44,9 @@ constexpr int kTileKeys = 32;       // keys per LDS tile (two 16-token pages)
 // wait on the LDS reads a full drain).  A split is at most this many pages.
 constexpr int kMaxSplitPages = 2048;
 constexpr float kLn2 = 0.69314718055994530942f;
-constexpr float kRescaleSlack = 8.0f;  // log2 units
+// A column's running sum may reach this before its reference max is raised
+// (every term 2^(s - m) is then at most 2^64, far inside fp32).
+constexpr float kSumLimit = 18446744073709551616.0f;  // 2^64
 
 struct AttnArgs {
   const uint16_t* q;      // [B, W, Hq, D]
@@ -380,17 +386,20 @@ void window_attn_kernel(AttnArgs a) {
     for (int m = 0; m < NM; ++m)
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[q][m][e] = 0.f;
-  float m_run[QB], l_run[QB];   // running max (raw score units), sum
+  // Per query column: m2 the reference max of s*c (log2 units; -inf before
+  // any score), l_run the running sum of the weights.
+  float m2[QB], l_run[QB];
 #pragma unroll
   for (int q = 0; q < QB; ++q) {
-    m_run[q] = kNegInf;
+    m2[q] = kNegInf;
     l_run[q] = 0.f;
   }
-  const float slack = kRescaleSlack / a.scale_log2;
+  const float c2 = a.scale_log2;
 
-  // ---- the three phases of one tile
+  // ---- the phases of one tile
   const int krow = key_of_row(col);
-  // S^T for this wave's query columns from the K tile at stage sb
+  // S^T for this wave's query columns from the K tile at stage sb, plain
+  // (accumulator from zero)
   auto qk = [&](int slot, floatx16_t (&sc)[QB]) {
     const char* sb = kb(slot);
 #pragma unroll
@@ -408,15 +417,58 @@ void window_attn_kernel(AttnArgs a) {
                                                         0, 0, 0);
     }
   };
-  // online softmax, first half: mask, tile max, lazily raised running
-  // max (rescaling O and l when it rises by more than the slack).  Returns
-  // the scaled max m*c that the exponentials subtract.
-  auto softmax_max = [&](floatx16_t (&sc)[QB], bool need_mask, int base,
-                         int lim_pre, bool is_win, float (&mc)[QB]) {
+  // Max over a column's 32 keys: 16 in this lane (a tree of v_max3), 16 in
+  // the lane 32 away.
+  auto col_max = [&](const floatx16_t& x) {
+    float t[6];
+#pragma unroll
+    for (int g = 0; g < 5; ++g)
+      t[g] = fmaxf(x[3 * g], fmaxf(x[3 * g + 1], x[3 * g + 2]));
+    t[5] = x[15];
+    float mx = fmaxf(t[0], fmaxf(t[1], t[2]));
+    mx = fmaxf(mx, fmaxf(t[3], t[4]));
+    mx = fmaxf(mx, t[5]);
+    float x0, x1;
+    xor32_pair(mx, x0, x1);
+    return fmaxf(x0, x1);
+  };
+  // Scale the column's partial output and sum by alpha.
+  auto rescale = [&](int q, float alpha) {
+    l_run[q] *= alpha;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[q][m][e] *= alpha;
+  };
+  // p = 2^(s*c - m2) for the 16 scores of this lane, P^T in bf16 (the B
+  // operands of the two 16-key P.V MFMAs) and l_run + the sum of the 16
+  // weights (a tree of fp32 adds).
+  auto exp_tile = [&](const floatx16_t (&x)[QB], bf16x8_t (&pf)[QB][2],
+                      float (&lsum)[QB]) {
 #pragma unroll
     for (int q = 0; q < QB; ++q) {
-      // the running max m_run stays in raw score units; the softmax scale
-      // enters once per element through p = 2^(s*c - m*c)
+      const float mc = m2[q] == kNegInf ? 0.f : m2[q];
+      float pe[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        pe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[q][e], c2, -mc));
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        pf[q][e >> 3][e & 7] = static_cast<__bf16>(pe[e]);
+      float ps[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        ps[g] = (pe[4 * g] + pe[4 * g + 1]) + (pe[4 * g + 2] + pe[4 * g + 3]);
+      lsum[q] = l_run[q] + ((ps[0] + ps[1]) + (ps[2] + ps[3]));
+    }
+  };
+  // Boundary tiles: masked keys set to -inf, the reference max raised to
+  // the tile's max where that is larger (rescaling the column), then the
+  // weights as above.
+  auto softmax_general = [&](floatx16_t (&sc)[QB], bool need_mask, int base,
+                             int lim_pre, bool is_win, bf16x8_t (&pf)[QB][2]) {
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
       if (need_mask) {
         const int lim = is_win ? min(a.W - 1, qi[q]) : lim_pre;
 #pragma unroll
@@ -425,62 +477,31 @@ void window_attn_kernel(AttnArgs a) {
           sc[q][e] = key <= lim ? sc[q][e] : kNegInf;
         }
       }
-      // three-input max tree: 16 scores in 8 v_max3
-      float t[6];
-#pragma unroll
-      for (int g = 0; g < 5; ++g)
-        t[g] = fmaxf(sc[q][3 * g], fmaxf(sc[q][3 * g + 1], sc[q][3 * g + 2]));
-      t[5] = sc[q][15];
-      float mx = fmaxf(t[0], fmaxf(t[1], t[2]));
-      mx = fmaxf(mx, fmaxf(t[3], t[4]));
-      mx = fmaxf(mx, t[5]);
-      {
-        float x0, x1;
-        xor32_pair(mx, x0, x1);
-        mx = fmaxf(x0, x1);
+      const float mx = col_max(sc[q]) * c2;
+      if (ballot(mx > m2[q])) {
+        const float m_new = fmaxf(m2[q], mx);
+        rescale(q, m2[q] == kNegInf ? 0.f
+                                    : __builtin_amdgcn_exp2f(m2[q] - m_new));
+        m2[q] = m_new;
       }
-      if (ballot(mx > m_run[q] + slack)) {
-        const float m_new = fmaxf(m_run[q], mx);
-        const float alpha =
-            (m_run[q] == kNegInf)
-                ? 0.f
-                : __builtin_amdgcn_exp2f((m_run[q] - m_new) * a.scale_log2);
-        l_run[q] *= alpha;
-#pragma unroll
-        for (int m = 0; m < NM; ++m)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[q][m][e] *= alpha;
-        m_run[q] = m_new;
-      }
-      mc[q] = (m_run[q] == kNegInf) ? 0.f : m_run[q] * a.scale_log2;
     }
+    float ls[QB];
+    exp_tile(sc, pf, ls);
+#pragma unroll
+    for (int q = 0; q < QB; ++q) l_run[q] = ls[q];
   };
-  // second half: p = 2^(s*c - m*c), the row sum, and P^T in bf16 as the B
-  // operand of the two 16-key P.V MFMAs.  Straight-line VALU only.
-  auto softmax_exp = [&](const floatx16_t (&sc)[QB], const float (&mc)[QB],
-                         bf16x8_t (&pf)[QB][2]) {
+  // Full tiles whose running sum passed kSumLimit (some 2^(s*c - m) is
+  // large): raise each column's reference max by the excess of its tile
+  // max over it, rescale, and take the weights again.
+  auto raise_max = [&](const floatx16_t (&sc)[QB], bf16x8_t (&pf)[QB][2],
+                       float (&lsum)[QB]) {
 #pragma unroll
     for (int q = 0; q < QB; ++q) {
-      float pe[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        pe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[q][e], a.scale_log2, -mc[q]));
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pf[q][h2][e] = static_cast<__bf16>(pe[h2 * 8 + e]);
-      float ps[4];
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-        ps[g] = (pe[4 * g] + pe[4 * g + 1]) + (pe[4 * g + 2] + pe[4 * g + 3]);
-      l_run[q] += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+      const float d = fmaxf(col_max(sc[q]) * c2 - m2[q], 0.f);
+      rescale(q, __builtin_amdgcn_exp2f(-d));
+      m2[q] += d;
     }
-  };
-  auto softmax = [&](floatx16_t (&sc)[QB], bool need_mask, int base,
-                     int lim_pre, bool is_win, bf16x8_t (&pf)[QB][2]) {
-    float mc[QB];
-    softmax_max(sc, need_mask, base, lim_pre, is_win, mc);
-    softmax_exp(sc, mc, pf);
+    exp_tile(sc, pf, lsum);
   };
   // V^T fragments of a tile: the A operands of the P.V MFMAs.  Row
   // m*32 + col keeps the swizzle bit of row col, so every fragment is this
@@ -510,7 +531,7 @@ void window_attn_kernel(AttnArgs a) {
 
   // ---- full prefix tiles.  Tile t lives in LDS slot t % NS and is loaded
   // LEAD iterations before the one that scores it.  Iteration t runs the
-  // softmax of tile t (VALU) under the score MFMAs of tile t+1, then the
+  // weights of tile t (VALU) under the score MFMAs of tile t+1, then the
   // P.V MFMAs of tile t, and issues the loads of tile t+LEAD.  The K
   // fragments run one step ahead: those of tile t+2 are read as soon as
   // the score MFMAs of tile t+1 have taken theirs, so the next iteration's
@@ -543,10 +564,10 @@ void window_attn_kernel(AttnArgs a) {
   // Tiles published at a barrier: with the K fragments one step ahead and
   // a barrier every two iterations, every tile up to t+4; without them and
   // a barrier every iteration, every tile up to t+2.
-  constexpr int kHorizon = kHoist ? 4 : 2;
+  constexpr int kHorizon = kBarEvery + (kHoist ? 2 : 1);
   constexpr int kInFlight = CPT * (LEAD - kHorizon);   // younger loads
   static_assert(LEAD > kHorizon, "publish horizon");
-  static_assert(kHoist ? NS >= LEAD + 2 : NS >= LEAD + 1, "slot reuse");
+  static_assert(NS >= LEAD + kBarEvery, "slot reuse");
   // K fragments of the next tile to score
   bf16x8_t kf[NK];
   auto kread = [&](int slot) {
@@ -565,6 +586,9 @@ void window_attn_kernel(AttnArgs a) {
     __syncthreads();
     qk(0, sbuf[0]);
     if constexpr (kHoist) kread(1);
+    // the first tile's max is each column's reference max
+#pragma unroll
+    for (int q = 0; q < QB; ++q) m2[q] = col_max(sbuf[0][q]) * c2;
   }
   // page ids of the next load, read one iteration ahead of their use
   int2 nid = ids_of(min(LEAD, max(last_full, 0)));
@@ -581,26 +605,33 @@ void window_attn_kernel(AttnArgs a) {
       nid = ids_of(min(t + LEAD + 1, last_full));                         \
       dma_ids(cur, (j + LEAD) % NS);                                      \
     }                                                                     \
-    float mc[QB];                                                         \
-    softmax_max(sbuf[j & 1], false, 0, 0, false, mc);                     \
-    /* one scheduling region: the score MFMAs of tile t+1 interleaved with */\
-    /* the exponentials of tile t                                          */\
+    /* one scheduling region: the score MFMAs of tile t+1 interleaved     */\
+    /* with the weights of tile t                                        */\
     bf16x8_t pf[QB][2];                                                   \
+    float lsum[QB];                                                       \
     _Pragma("unroll")                                                     \
     for (int q = 0; q < QB; ++q) {                                        \
+      sbuf[(j + 1) & 1][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(     \
+          kf[0], qf[q][0], floatx16_t{}, 0, 0, 0);                        \
       _Pragma("unroll")                                                   \
-      for (int e = 0; e < 16; ++e) sbuf[(j + 1) & 1][q][e] = 0.f;         \
-      _Pragma("unroll")                                                   \
-      for (int kk = 0; kk < NK; ++kk)                                     \
+      for (int kk = 1; kk < NK; ++kk)                                     \
         sbuf[(j + 1) & 1][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(   \
             kf[kk], qf[q][kk], sbuf[(j + 1) & 1][q], 0, 0, 0);            \
     }                                                                     \
-    softmax_exp(sbuf[j & 1], mc, pf);                                     \
+    exp_tile(sbuf[j & 1], pf, lsum);                                      \
     _Pragma("unroll")                                                     \
     for (int i = 0; i < NK * QB; ++i) {                                   \
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   /* one MFMA  */\
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   /* six VALU  */\
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   /* four VALU */\
     }                                                                     \
+    {                                                                     \
+      bool big = false;                                                   \
+      _Pragma("unroll")                                                   \
+      for (int q = 0; q < QB; ++q) big = big || (lsum[q] > kSumLimit);    \
+      if (ballot(big)) raise_max(sbuf[j & 1], pf, lsum);                  \
+    }                                                                     \
+    _Pragma("unroll")                                                     \
+    for (int q = 0; q < QB; ++q) l_run[q] = lsum[q];                      \
     /* K fragments of tile t+2 (a re-read tile past the last full one) */ \
     if constexpr (kHoist) kread((j + 2) % NS);                            \
     pv(vf, pf);                                                           \
@@ -712,7 +743,7 @@ tiles_done:
     __syncthreads();
     qk(ts, sbuf[0]);
     bf16x8_t pf[QB][2], vf[2][NM];
-    softmax(sbuf[0], true, base, lim, is_win, pf);
+    softmax_general(sbuf[0], true, base, lim, is_win, pf);
     vread(ts, vf);
     pv(vf, pf);
   }
@@ -746,7 +777,7 @@ tiles_done:
         }
       if (a.lse && hf == 0)
         a.lse[(static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]] =
-            (m_run[q] * a.scale_log2 + __log2f(l_tot)) * kLn2;
+            (m2[q] + __log2f(l_tot)) * kLn2;
     } else {
       float* wp = a.ws_o + (rows_base * a.nsplit + split) * D;
 #pragma unroll
@@ -760,7 +791,7 @@ tiles_done:
         }
       if (hf == 0)
         a.ws_ml[rows_base * a.nsplit + split] =
-            make_float2(m_run[q] * a.scale_log2, l_tot);   // log2 units
+            make_float2(m2[q], l_tot);   // log2 units
     }
   }
 }

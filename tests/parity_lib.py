@@ -122,7 +122,9 @@ def check_reorder(wl, g, o):
         assert (O.bf16_to_f64(g["v_phys"][b]) == o[b]["v"]).all(), b
 
 
-def check_attention(wl, g, o, seqs):
+def check_attention(wl, g, o, seqs, lse_bound=None):
+    """lse_bound(b): per (row, head) bound on |lse - lse_ref| (default
+    2e-2 everywhere)."""
     worst_abs, num, den, n = 0.0, 0.0, 0.0, 0
     for b in seqs:
         rr, hh = o[b]["attn_rows"], o[b]["attn_heads"]
@@ -134,7 +136,8 @@ def check_attention(wl, g, o, seqs):
         den += float((ref ** 2).sum())
         n += err.size
         glse = g["lse"][b][np.ix_(rr, hh)]
-        assert np.abs(glse - o[b]["lse"]).max() < 2e-2, b
+        bound = 2e-2 if lse_bound is None else lse_bound(b)
+        assert (np.abs(glse - o[b]["lse"]) < bound).all(), b
         assert int(g["attn_status"][b]) == 0, b
     rel = math.sqrt(num / max(den, 1e-300))
     log(f"  attention: {n} values, max abs {worst_abs:.3e}, rel norm {rel:.3e}")

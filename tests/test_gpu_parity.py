@@ -104,6 +104,92 @@ def test_four_wave_two_per_cu_tile_counts():
     _full_check(wl, d, list(range(len(lens))) + [40, 63])
 
 
+def _lift_scores_from(wl, d, start, alpha):
+    """Scores that jump far above the first tile's: coordinate j = D/2 - 1 of
+    every query is set to 4 (its RoPE pair turns by under 0.01 rad at these
+    positions, so it stays near 4 after rotation), and alpha is added to
+    that coordinate of the cached keys of every prefix position >= start
+    (bf16).  Every query then scores those keys about 4 * alpha / sqrt(D)
+    higher, in common, while the spread among them stays that of the
+    original keys: the softmax is well conditioned, however large alpha."""
+    j = wl.D // 2 - 1
+    qkv = d["qkv_in"]
+    qkv[:, :, :wl.Hq, j] = WL.f32_to_bf16_bits(np.float32(4.0))
+    k = d["k_cache"]
+    bt = d["block_table"]
+    for b in range(bt.shape[0]):
+        c = int(d["win_start"][b])
+        for pos in range(start - start % WL.PAGE, c, WL.PAGE):
+            pg = int(bt[b, pos // WL.PAGE])
+            lo = max(start - pos, 0)
+            f = (k[pg, :, lo:, j].astype(np.uint32) << 16).view(np.float32)
+            k[pg, :, lo:, j] = WL.f32_to_bf16_bits(f + np.float32(alpha))
+
+
+def _grow_check(wl, d, seqs, rows=None, heads=None):
+    """A full step check whose lse bound follows from the inputs: the kernel
+    scores with queries rounded to bf16 twice (the rotation's output, then
+    the pre-scaled copy), each rounding at most 2^-8 relative (half an ulp
+    at the bottom of a binade), so its scores and lse are within
+    2^-7 * max_k sum_i |q_i k_i| / sqrt(D) of the oracle's (lse moves by at
+    most the largest score change)."""
+    PL.log(f"case {wl.name}: B={wl.B} W={wl.W} Hq={wl.Hq} Hkv={wl.Hkv} "
+           f"D={wl.D} c={list(d['win_start'][:4])}")
+    g, step, dev = PL.run_gpu_step(wl, d)
+    o = PL.oracle_step(wl, d, seqs, rows, heads)
+
+    def lse_bound(b):
+        from oracle import wedlm_oracle as O
+        c = int(d["win_start"][b])
+        kp, _ = WL.gather_prefix(d["k_cache"], d["v_cache"], d["block_table"],
+                                 b, c)
+        keys = np.concatenate([O.bf16_to_f64(kp), o[b]["k"]], axis=0)
+        q = o[b]["q"]
+        rr, hh = o[b]["attn_rows"], o[b]["attn_heads"]
+        out = np.zeros((len(rr), len(hh)))
+        for hi, h in enumerate(hh):
+            ak = np.abs(keys[:, h // wl.G, :])
+            for ri, i in enumerate(rr):
+                m = (ak[:c + i + 1] @ np.abs(q[i, h])).max()
+                out[ri, hi] = 2e-2 + 2.0 ** -7 * m / np.sqrt(wl.D)
+        return out
+
+    PL.check_reorder(wl, g, o)
+    PL.check_attention(wl, g, o, seqs, lse_bound)
+    PL.check_score(wl, d, g, o)
+    PL.check_commit(wl, d, g, o)
+    PL.check_append(wl, dev, g, o)
+
+
+@pytest.mark.parametrize("alpha", [200.0, 2000.0])
+def test_scores_growing_past_first_tile(alpha):
+    """Keys of prefix positions from 64 on lifted by about 70 nats (alpha
+    200: past the 64 log2 units the running sum tolerates) or 700 nats
+    (alpha 2000: 2^s overflows fp32) above the first two tiles: the kernel
+    must raise the reference max, rescale, and shift the in-flight next
+    tile.  Sequences of 600-1200 positions split four ways, so one split
+    meets the jump inside its range and the others start above it."""
+    wl = WL.Workload(f"grow{int(alpha)}", 73, B=3, W=16, Hq=8, Hkv=2, D=128,
+                     V=400, prefix=600, prefix_hi=1200, obs_frac=0.0,
+                     obs_frac_hi=0.75, spike=9.0, spike_prob=0.5)
+    d = WL.step_inputs(wl, seed=0)
+    _lift_scores_from(wl, d, 64, alpha)
+    _grow_check(wl, d, list(range(wl.B)))
+
+
+def test_scores_growing_two_per_cu():
+    """The same jump on the four-wave two-per-CU kernel (128 query rows per
+    kv head, 512 workgroups), whose exponent arguments subtract the
+    reference max per score instead of seeding the MFMA accumulators."""
+    wl = WL.Workload("grow_two", 74, B=64, W=32, Hq=32, Hkv=8, D=128,
+                     V=300, prefix=200, prefix_hi=330, obs_frac=0.0,
+                     obs_frac_hi=0.75, spike=9.0, spike_prob=0.5)
+    d = WL.step_inputs(wl, seed=0)
+    _lift_scores_from(wl, d, 64, 2000.0)
+    _grow_check(wl, d, [0, 1, 33, 63], lambda b, n: _sample_rows(b, n, wl.W),
+                lambda b: sorted({0, 3, 4, 31, (5 * b) % 32}))
+
+
 def test_prefix_beyond_one_split_of_pages():
     """A prefix longer than one split's staged page ids (2048 pages, 32,768
     positions) on a grid that already fills the CUs (16 sequences x 16 kv
