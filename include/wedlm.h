@@ -69,7 +69,8 @@ enum {
   WEDLM_E_SHAPE = -2,     /* unsupported or inconsistent shape              */
   WEDLM_E_WORKSPACE = -3, /* workspace smaller than the *_workspace_size()  */
   WEDLM_E_LAUNCH = -4,    /* a kernel launch failed                         */
-  WEDLM_E_DEVICE = -5     /* no usable gfx950 device                        */
+  WEDLM_E_DEVICE = -5,    /* no usable gfx950 device                        */
+  WEDLM_E_SCRATCH = -6    /* needs more than the library's fixed scratch    */
 };
 
 /* per-sequence status bits (int32 status[B]); 0 = fine */
@@ -160,6 +161,35 @@ int wedlm_window_attn(const uint16_t* q_phys, const uint16_t* k_phys,
                       int32_t max_prefix_len, float softmax_scale,
                       uint16_t* out, float* lse, int32_t* status,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * wedlm_window_attn_noalloc -- wedlm_window_attn for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, operation,
+ * layouts and results as wedlm_window_attn, without the workspace: the
+ * split-K partials go to a scratch array of WEDLM_ATTN_SCRATCH_BYTES that
+ * the library holds in each device's memory from load to process exit.
+ * Nothing is allocated or freed by the call.
+ *
+ * Limit: the call's workspace need, wedlm_window_attn_workspace_size(B, W,
+ * Hq, Hkv, D, max_prefix_len), must not exceed WEDLM_ATTN_SCRATCH_BYTES
+ * (64 MiB: e.g. 8 sequences x 8 kv heads x 256 query rows over 4 splits at
+ * D = 128 need 34 MiB); otherwise WEDLM_E_SCRATCH and nothing is enqueued.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents (nothing in it needs to start at zero): calls that overlap on
+ * one GPU (other streams, other threads) race and must be serialised by the
+ * caller.  WEDLM_E_DEVICE if the array's device address cannot be obtained.
+ */
+#define WEDLM_ATTN_SCRATCH_BYTES ((size_t)64 << 20)
+int wedlm_window_attn_noalloc(const uint16_t* q_phys, const uint16_t* k_phys,
+                              const uint16_t* v_phys, const uint16_t* k_cache,
+                              const uint16_t* v_cache, int64_t num_pages,
+                              const int32_t* block_table, int32_t max_pages,
+                              const int32_t* prefix_len, int32_t B, int32_t W,
+                              int32_t Hq, int32_t Hkv, int32_t D,
+                              int32_t max_prefix_len, float softmax_scale,
+                              uint16_t* out, float* lse, int32_t* status,
+                              void* stream);
 
 /*
  * wedlm_score -- per mask slot, the greedy token and the entropy of the

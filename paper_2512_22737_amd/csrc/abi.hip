@@ -9,6 +9,8 @@ extern "C" const char* wedlm_strerror(int code) {
     case WEDLM_E_WORKSPACE: return "workspace too small";
     case WEDLM_E_LAUNCH: return "kernel launch failed";
     case WEDLM_E_DEVICE: return "no usable gfx950 device";
+    case WEDLM_E_SCRATCH:
+      return "needs more than the library's fixed scratch array";
     default: return "unknown error code";
   }
 }

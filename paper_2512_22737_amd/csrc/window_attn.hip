@@ -34,6 +34,8 @@
 // arithmetic intensity of W*G flop/byte (256 at W=64, G=4).
 #include "common.h"
 
+#include <mutex>
+
 using namespace wedlm;
 
 namespace {
@@ -918,23 +920,25 @@ extern "C" size_t wedlm_window_attn_workspace_size(int32_t B, int32_t W,
   return make_plan(B, W, Hq, Hkv, D, max_prefix_len).ws_bytes;
 }
 
-extern "C" int wedlm_window_attn(
+// Split-K partials of wedlm_window_attn_noalloc: one array per device (each
+// GPU the library runs on holds its own copy until the process ends).  In
+// host code the name is only a handle, never a device address: the address
+// comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) char scratch[WEDLM_ATTN_SCRATCH_BYTES];
+
+namespace {
+
+constexpr size_t kScratchBytes = WEDLM_ATTN_SCRATCH_BYTES;
+
+// The entry point's work; `workspace` holds at least the plan's bytes
+// (checked by the callers).
+int window_attn_impl(
     const uint16_t* q_phys, const uint16_t* k_phys, const uint16_t* v_phys,
     const uint16_t* k_cache, const uint16_t* v_cache, int64_t num_pages,
     const int32_t* block_table, int32_t max_pages, const int32_t* prefix_len,
     int32_t B, int32_t W, int32_t Hq, int32_t Hkv, int32_t D,
     int32_t max_prefix_len, float softmax_scale, uint16_t* out, float* lse,
-    int32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
-  if (!q_phys || !k_phys || !v_phys || !block_table || !prefix_len || !out)
-    return WEDLM_E_ARG;
-  if (!shape_ok(B, W, Hq, Hkv, D, max_prefix_len)) return WEDLM_E_SHAPE;
-  if (max_prefix_len > 0 && (!k_cache || !v_cache || num_pages < 1 ||
-                             max_pages < 1))
-    return WEDLM_E_ARG;
-  if (!(softmax_scale > 0.f) || !(softmax_scale < 1e30f)) return WEDLM_E_ARG;
-  const Plan p = make_plan(B, W, Hq, Hkv, D, max_prefix_len);
-  if (workspace_bytes < p.ws_bytes || (p.ws_bytes && !workspace))
-    return WEDLM_E_WORKSPACE;
+    int32_t* status, const Plan& p, void* workspace, hipStream_t st) {
   AttnArgs a{};
   a.q = q_phys; a.kw = k_phys; a.vw = v_phys; a.kc = k_cache; a.vc = v_cache;
   a.bt = block_table; a.plen = prefix_len; a.out = out; a.lse = lse;
@@ -952,6 +956,89 @@ extern "C" int wedlm_window_attn(
     size_t off = (n * D * sizeof(float) + 255) & ~static_cast<size_t>(255);
     a.ws_ml = reinterpret_cast<float2*>(base + off);
   }
-  hipStream_t st = static_cast<hipStream_t>(stream);
   return D == 128 ? launch<128>(a, p, st) : launch<64>(a, p, st);
+}
+
+// Host-side checks shared by both entry points.
+int check_args(const uint16_t* q_phys, const uint16_t* k_phys,
+               const uint16_t* v_phys, const uint16_t* k_cache,
+               const uint16_t* v_cache, int64_t num_pages,
+               const int32_t* block_table, int32_t max_pages,
+               const int32_t* prefix_len, int32_t B, int32_t W, int32_t Hq,
+               int32_t Hkv, int32_t D, int32_t max_prefix_len,
+               float softmax_scale, const uint16_t* out) {
+  if (!q_phys || !k_phys || !v_phys || !block_table || !prefix_len || !out)
+    return WEDLM_E_ARG;
+  if (!shape_ok(B, W, Hq, Hkv, D, max_prefix_len)) return WEDLM_E_SHAPE;
+  if (max_prefix_len > 0 && (!k_cache || !v_cache || num_pages < 1 ||
+                             max_pages < 1))
+    return WEDLM_E_ARG;
+  if (!(softmax_scale > 0.f) || !(softmax_scale < 1e30f)) return WEDLM_E_ARG;
+  return WEDLM_OK;
+}
+
+constexpr int kMaxDevices = 64;
+void* g_scratch_ptr[kMaxDevices];
+std::once_flag g_scratch_once[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// Device address of this device's scratch array (nullptr on failure).
+void* scratch_ptr(int dev) {
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* ptr = nullptr;
+    g_scratch_err[dev] =
+        hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? ptr : nullptr;
+  });
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" int wedlm_window_attn_noalloc(
+    const uint16_t* q_phys, const uint16_t* k_phys, const uint16_t* v_phys,
+    const uint16_t* k_cache, const uint16_t* v_cache, int64_t num_pages,
+    const int32_t* block_table, int32_t max_pages, const int32_t* prefix_len,
+    int32_t B, int32_t W, int32_t Hq, int32_t Hkv, int32_t D,
+    int32_t max_prefix_len, float softmax_scale, uint16_t* out, float* lse,
+    int32_t* status, void* stream) {
+  const int e = check_args(q_phys, k_phys, v_phys, k_cache, v_cache,
+                           num_pages, block_table, max_pages, prefix_len, B,
+                           W, Hq, Hkv, D, max_prefix_len, softmax_scale, out);
+  if (e != WEDLM_OK) return e;
+  const Plan p = make_plan(B, W, Hq, Hkv, D, max_prefix_len);
+  if (p.ws_bytes > kScratchBytes) return WEDLM_E_SCRATCH;
+  void* ws = nullptr;
+  if (p.ws_bytes) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+      return WEDLM_E_DEVICE;
+    ws = scratch_ptr(dev);
+    if (!ws) return WEDLM_E_DEVICE;
+  }
+  return window_attn_impl(q_phys, k_phys, v_phys, k_cache, v_cache,
+                          num_pages, block_table, max_pages, prefix_len, B, W,
+                          Hq, Hkv, D, max_prefix_len, softmax_scale, out, lse,
+                          status, p, ws, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int wedlm_window_attn(
+    const uint16_t* q_phys, const uint16_t* k_phys, const uint16_t* v_phys,
+    const uint16_t* k_cache, const uint16_t* v_cache, int64_t num_pages,
+    const int32_t* block_table, int32_t max_pages, const int32_t* prefix_len,
+    int32_t B, int32_t W, int32_t Hq, int32_t Hkv, int32_t D,
+    int32_t max_prefix_len, float softmax_scale, uint16_t* out, float* lse,
+    int32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
+  const int e = check_args(q_phys, k_phys, v_phys, k_cache, v_cache,
+                           num_pages, block_table, max_pages, prefix_len, B,
+                           W, Hq, Hkv, D, max_prefix_len, softmax_scale, out);
+  if (e != WEDLM_OK) return e;
+  const Plan p = make_plan(B, W, Hq, Hkv, D, max_prefix_len);
+  if (workspace_bytes < p.ws_bytes || (p.ws_bytes && !workspace))
+    return WEDLM_E_WORKSPACE;
+  return window_attn_impl(q_phys, k_phys, v_phys, k_cache, v_cache,
+                          num_pages, block_table, max_pages, prefix_len, B, W,
+                          Hq, Hkv, D, max_prefix_len, softmax_scale, out, lse,
+                          status, p, workspace,
+                          static_cast<hipStream_t>(stream));
 }

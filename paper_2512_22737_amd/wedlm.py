@@ -53,6 +53,10 @@ def _load():
                                       I32, I32, I32, I32, F, P, P, P, P, SZ,
                                       P]
     lib.wedlm_window_attn.restype = ctypes.c_int
+    lib.wedlm_window_attn_noalloc.argtypes = [P, P, P, P, P, I64, P, I32, P,
+                                              I32, I32, I32, I32, I32, I32, F,
+                                              P, P, P, P]
+    lib.wedlm_window_attn_noalloc.restype = ctypes.c_int
     lib.wedlm_score_workspace_size.argtypes = [I32, I32, I32]
     lib.wedlm_score_workspace_size.restype = SZ
     lib.wedlm_score.argtypes = [P, I64, P, I32, I32, I32, D_, P, P, P, P, SZ,
@@ -111,7 +115,8 @@ def lib():
 
 
 EXPORTED = ["wedlm_reorder", "wedlm_window_attn_workspace_size",
-            "wedlm_window_attn", "wedlm_score_workspace_size", "wedlm_score",
+            "wedlm_window_attn", "wedlm_window_attn_noalloc",
+            "wedlm_score_workspace_size", "wedlm_score",
             "wedlm_commit", "wedlm_commit_rule",
             "wedlm_lm_head_score_workspace_size", "wedlm_lm_head_score",
             "wedlm_strerror", "wedlm_version", "wedlm_embed", "wedlm_rmsnorm",
@@ -226,6 +231,33 @@ def wedlm_window_attn(q_phys, k_phys, v_phys, k_cache, v_cache, block_table,
         _t(status, "status", i32, (B,), allow_none=True), ws_ptr, ws_bytes,
         _stream())
     _check(code, "wedlm_window_attn")
+
+
+def wedlm_window_attn_noalloc(q_phys, k_phys, v_phys, k_cache, v_cache,
+                              block_table, prefix_len, max_prefix_len: int,
+                              out, lse=None, status=None,
+                              softmax_scale: Optional[float] = None) -> None:
+    """wedlm_window_attn with the library's own scratch array in place of a
+    workspace (include/wedlm.h); nothing is allocated."""
+    B, W, Hq, D = q_phys.shape
+    Hkv = k_phys.shape[2]
+    P = k_cache.shape[0]
+    maxp = block_table.shape[1]
+    if softmax_scale is None:
+        softmax_scale = 1.0 / math.sqrt(D)
+    i32 = (torch.int32,)
+    code = _load().wedlm_window_attn_noalloc(
+        _t(q_phys, "q_phys", _BF16), _t(k_phys, "k_phys", _BF16, (B, W, Hkv, D)),
+        _t(v_phys, "v_phys", _BF16, (B, W, Hkv, D)),
+        _t(k_cache, "k_cache", _BF16, (P, Hkv, PAGE_SIZE, D)),
+        _t(v_cache, "v_cache", _BF16, (P, Hkv, D, PAGE_SIZE)), P,
+        _t(block_table, "block_table", i32, (B, maxp)), maxp,
+        _t(prefix_len, "prefix_len", i32, (B,)), B, W, Hq, Hkv, D,
+        int(max_prefix_len), float(softmax_scale),
+        _t(out, "out", _BF16, (B, W, Hq, D)),
+        _t(lse, "lse", (torch.float32,), (B, W, Hq), allow_none=True),
+        _t(status, "status", i32, (B,), allow_none=True), _stream())
+    _check(code, "wedlm_window_attn_noalloc")
 
 
 def wedlm_score_workspace_size(B, W, V) -> int:
