@@ -291,7 +291,6 @@ int wedlm_commit_rule(int32_t* win_tok, int32_t* win_start,
                       uint8_t* selected, int32_t* status, int32_t rule,
                       void* stream);
 
-/* Message for a WEDLM_* return code (static storage). */
 /*
  * wedlm_lm_head_score -- the output layer of the window forward fused with
  * the score of its rows: the logits that the mask slots are scored on
@@ -323,6 +322,7 @@ int wedlm_lm_head_score(const uint16_t* hidden, const uint16_t* w_vocab,
                         void* workspace, size_t workspace_bytes,
                         void* stream);
 
+/* Message for a WEDLM_* return code (static storage). */
 const char* wedlm_strerror(int code);
 
 /* Library version, major * 10000 + minor * 100 + patch. */

@@ -188,25 +188,28 @@ def near_threshold(wl, o_b) -> bool:
 
 
 def check_commit(wl, d, g, o):
+    """Commit count, committed tokens and slots, status and the new prefix
+    length depend on no entropy and are always compared bit-exactly.  The
+    selection and the refilled window are compared bit-exactly too, except
+    on sequences whose decision sits within NEAR of a threshold, which are
+    counted and reported."""
     near = 0
     for b in range(wl.B):
         cm = o[b]["commit"]
-        same = (int(g["n_commit"][b]) == cm["n"] and
-                list(g["selected"][b]) == cm["selected"] and
-                list(g["win_tok"][b]) == cm["win"] and
-                int(g["win_start"][b]) == cm["c"])
-        if not same and near_threshold(wl, o[b]):
-            near += 1
-            continue
         assert int(g["status"][b]) == 0, b
         assert int(g["n_commit"][b]) == cm["n"], b
         n = cm["n"]
         assert list(g["committed_tok"][b][:n]) == cm["committed"], b
         assert list(g["committed_slot"][b][:n]) == cm["slots"], b
         assert (g["committed_tok"][b][n:] == -1).all()
+        assert int(g["win_start"][b]) == cm["c"], b
+        same = (list(g["selected"][b]) == cm["selected"] and
+                list(g["win_tok"][b]) == cm["win"])
+        if not same and near_threshold(wl, o[b]):
+            near += 1
+            continue
         assert list(g["selected"][b]) == cm["selected"], b
         assert list(g["win_tok"][b]) == cm["win"], b
-        assert int(g["win_start"][b]) == cm["c"], b
     log(f"  commit: {wl.B} sequences, near-threshold mismatches {near}")
     return near
 

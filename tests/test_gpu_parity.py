@@ -273,8 +273,8 @@ def test_secondary_readings(lam, temp):
 
 def test_attention_workspace_reuse():
     """One workspace, three calls with shrinking prefixes (so the number of
-    prefix splits per sequence changes between calls): the split arrival
-    counters must come back to zero after each call."""
+    prefix splits per sequence changes between calls): partials a longer
+    call left in the workspace must not leak into a shorter one."""
     import torch
     from oracle import wedlm_oracle as O
     from paper_2512_22737_amd import wedlm
