@@ -64,7 +64,7 @@ struct AttnArgs {
   float* ws_o;            // [B, Hkv, rows_pad, nsplit, D]
   float2* ws_ml;          // [B, Hkv, rows_pad, nsplit]
   int64_t num_pages;
-  int B, W, Hq, Hkv, G, max_pages, max_prefix, nsplit, split_len, qblocks,
+  int B, W, Hq, Hkv, G, max_pages, max_prefix, nsplit, qblocks,
       rows_pad;
   float scale_log2;       // softmax_scale * log2(e)
 };
@@ -84,7 +84,7 @@ Shape pick_shape(int rows) {
 struct Plan {
   Shape sh;
   bool two;               // four-wave workgroups, two per CU
-  int rows, rows_per_wg, qblocks, rows_pad, nsplit, split_len;
+  int rows, rows_per_wg, qblocks, rows_pad, nsplit;
   size_t ws_bytes;
 };
 
@@ -98,21 +98,28 @@ Plan make_plan(int B, int W, int Hq, int Hkv, int D, int max_prefix) {
   p.rows_pad = p.qblocks * p.rows_per_wg;
   const int tiles = (max_prefix + kTileKeys - 1) / kTileKeys;
   const int base = B * Hkv * p.qblocks;
-  // one workgroup per CU; four-wave workgroups run two per CU when the
-  // grid has 512 without splitting (more splits cost more than they gain)
-  p.two = p.sh.nw == 4 && base >= 512;
-  const int target = 256;
-  int nsplit = (target + base - 1) / base;
   const int max_split = tiles / 8 > 1 ? tiles / 8 : 1;  // >= 8 tiles each
-  if (nsplit > max_split) nsplit = max_split;
+  // Four-wave workgroups run two per CU when the grid reaches 512 (every
+  // SIMD then holds two waves): without splitting, or by splitting when
+  // the prefix bound allows 32 tiles per split (shorter prefixes measured
+  // faster one workgroup per CU).  Otherwise about 256 workgroups.
+  p.two = false;
+  int nsplit = 1;
+  if (p.sh.nw == 4) {
+    const int need = (512 + base - 1) / base;
+    if (need == 1 || tiles >= 32 * need) {
+      p.two = true;
+      nsplit = need;
+    }
+  }
+  if (!p.two) {
+    nsplit = (256 + base - 1) / base;
+    if (nsplit > max_split) nsplit = max_split;
+  }
   if (nsplit < 1) nsplit = 1;
   const int min_split = (tiles + kMaxSplitPages / 2 - 1) / (kMaxSplitPages / 2);
   if (nsplit < min_split) nsplit = min_split;
-  int tiles_per = (tiles + nsplit - 1) / nsplit;
-  if (tiles_per < 1) tiles_per = 1;
-  p.split_len = tiles_per * kTileKeys;
-  p.nsplit = (max_prefix + p.split_len - 1) / p.split_len;
-  if (p.nsplit < 1) p.nsplit = 1;
+  p.nsplit = nsplit;
   if (p.nsplit == 1) {
     p.ws_bytes = 0;
   } else {
@@ -120,6 +127,27 @@ Plan make_plan(int B, int W, int Hq, int Hkv, int D, int max_prefix) {
     p.ws_bytes = n * D * sizeof(float) + 256 + n * sizeof(float2);
   }
   return p;
+}
+
+// Split of one sequence's prefix of c positions over the launch's nsplit
+// slots: as many splits as keep at least 8 tiles each (one for an empty
+// prefix), each of the same whole number of tiles.  Derived on the device
+// from the sequence's own c, so a max_prefix_len far above the prefixes in
+// use does not leave splits empty.  At most 1024 tiles per split (2048
+// staged page ids), since the plan takes nsplit >= max tiles / 1024.
+struct SeqSplit {
+  int n, len;             // splits in use, positions per split
+};
+
+__device__ __forceinline__ SeqSplit seq_split(int c, int nsplit) {
+  const int tiles = (c + kTileKeys - 1) / kTileKeys;
+  int n = tiles / 8;
+  n = n < 1 ? 1 : (n > nsplit ? nsplit : n);
+  const int per = tiles > 0 ? (tiles + n - 1) / n : 1;
+  SeqSplit r;
+  r.len = per * kTileKeys;
+  r.n = c > 0 ? (c + r.len - 1) / r.len : 1;
+  return r;
 }
 
 // Sequence validity; bad lengths are reported and the sequence skipped.
@@ -265,10 +293,11 @@ void window_attn_kernel(AttnArgs a) {
       atomicOr(a.status + b, WEDLM_SEQ_BAD_LEN);
     return;
   }
-  const int nsplit_b = c > 0 ? (c + a.split_len - 1) / a.split_len : 1;
+  const SeqSplit ss = seq_split(c, a.nsplit);
+  const int nsplit_b = ss.n;
   if (split >= nsplit_b) return;
-  const int k0 = split * a.split_len;
-  const int k1 = min(c, k0 + a.split_len);
+  const int k0 = split * ss.len;
+  const int k1 = min(c, k0 + ss.len);
   const bool last = split == nsplit_b - 1;
   const int n_pre = k1 > k0 ? (k1 - k0 + kTileKeys - 1) / kTileKeys : 0;
   const int n_win = last ? (a.W + kTileKeys - 1) / kTileKeys : 0;
@@ -818,7 +847,7 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
   const int b = bk / a.Hkv;
   int c;
   if (!seq_ok(a, b, c)) return;
-  const int nsplit_b = c > 0 ? (c + a.split_len - 1) / a.split_len : 1;
+  const int nsplit_b = seq_split(c, a.nsplit).n;
   const int d = (threadIdx.x % TPR) * 4;
   const int64_t rows_base =
       (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
@@ -946,7 +975,7 @@ int window_attn_impl(
   a.num_pages = num_pages;
   a.B = B; a.W = W; a.Hq = Hq; a.Hkv = Hkv; a.G = Hq / Hkv;
   a.max_pages = max_pages; a.max_prefix = max_prefix_len;
-  a.nsplit = p.nsplit; a.split_len = p.split_len; a.qblocks = p.qblocks;
+  a.nsplit = p.nsplit; a.qblocks = p.qblocks;
   a.rows_pad = p.rows_pad;
   a.scale_log2 = softmax_scale * 1.4426950408889634f;
   if (p.nsplit > 1) {

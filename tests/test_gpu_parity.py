@@ -190,6 +190,42 @@ def test_scores_growing_two_per_cu():
                 lambda b: sorted({0, 3, 4, 31, (5 * b) % 32}))
 
 
+def test_two_per_cu_with_prefix_splits():
+    """128 query rows per kv head on a grid of 128 (sequence, kv head)
+    pairs, with a prefix bound long enough to split four ways: the
+    four-wave kernel that runs two per CU over 512 workgroups.  Each
+    sequence splits its own prefix (0 to 4 splits in use: empty, short and
+    long prefixes); attention checked on sampled rows and heads."""
+    wl = WL.Workload("two_split", 75, B=16, W=32, Hq=32, Hkv=8, D=128, V=300,
+                     prefix=4200, prefix_hi=4200, obs_frac=0.0,
+                     obs_frac_hi=0.75, spike=9.0, spike_prob=0.5)
+    d = WL.step_inputs(wl, seed=0)
+    # the block tables and caches cover 4200 + W positions; shorter
+    # prefixes use a part
+    d["win_start"][:] = [0, 40, 255, 4200, 3000, 1000, 511, 2047, 256, 4100,
+                         17, 700, 1500, 2600, 3900, 4199]
+    _full_check(wl, d, [0, 1, 2, 3, 9], lambda b, n: _sample_rows(b, n, wl.W),
+                lambda b: sorted({0, 3, 4, 31, (5 * b) % 32}))
+
+
+def test_prefix_bound_far_above_the_prefixes():
+    """max_prefix_len four times the longest prefix (a serving loop sizes
+    its buffers for the whole run): the splits follow each sequence's own
+    prefix, and the results are those of a tight bound."""
+    wl = WL.Workload("slack", 76, B=6, W=64, Hq=8, Hkv=2, D=128, V=500,
+                     prefix=300, prefix_hi=3000, obs_frac=0.0,
+                     obs_frac_hi=0.75, spike=9.0, spike_prob=0.5)
+    d = WL.step_inputs(wl, seed=0, extra_positions=9000)
+    mp = 4 * int(d["win_start"].max())
+    PL.log(f"case slack: max_prefix {mp}")
+    g, step, dev = PL.run_gpu_step(wl, d, max_prefix=mp)
+    o = PL.oracle_step(wl, d, list(range(wl.B)))
+    PL.check_reorder(wl, g, o)
+    PL.check_attention(wl, g, o, list(range(wl.B)))
+    PL.check_score(wl, d, g, o)
+    PL.check_commit(wl, d, g, o)
+
+
 def test_prefix_beyond_one_split_of_pages():
     """A prefix longer than one split's staged page ids (2048 pages, 32,768
     positions) on a grid that already fills the CUs (16 sequences x 16 kv
