@@ -112,56 +112,71 @@ __device__ Run committed_run(const CommitArgs& a, int b) {
 // layers [l0, l1), 16-byte pieces of D/8 bf16 values, spread over the
 // workgroup's threads.  K rows are contiguous in both layouts.  For V the
 // lanes run over consecutive rows of one (head, 8 values of d), so the
-// transposed stores of one page land in contiguous 32-byte rows.
+// transposed stores of one page land in contiguous 32-byte rows.  Each
+// thread loads up to kAppendBatch pieces of K and of V before storing any,
+// so a batch costs one memory round trip.
+constexpr int kAppendBatch = 8;
+
 __device__ void append_rows(const CommitArgs& a, int b, int n, int c, int l0,
-                            int l1) {
+                            int l1, int h0, int h1) {
   const int W = a.W, D = a.D, Hkv = a.Hkv;
   const int DG = D / 8;
+  const int NH = h1 - h0;
   const int32_t* bt = a.bt + static_cast<int64_t>(b) * a.max_pages;
-  const int total = n * Hkv * DG;
-  for (int e2 = threadIdx.x; e2 < total * (l1 - l0); e2 += kThreads) {
-    const int l = l0 + e2 / total, e = e2 % total;
-    const uint16_t* k_phys = a.k_phys + l * a.win_lstride;
-    const uint16_t* v_phys = a.v_phys + l * a.win_lstride;
-    uint16_t* k_cache = a.k_cache + l * a.cache_lstride;
-    uint16_t* v_cache = a.v_cache + l * a.cache_lstride;
-    // K: e = (j, h, dg), dg fastest
-    {
-      const int dg = e % DG;
-      const int jh = e / DG;
-      const int h = jh % Hkv;
-      const int j = jh / Hkv;
-      const int p = c + j;
-      const int64_t pg = bt[p / kPage];
-      const int row = p % kPage;
-      const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
-          k_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
-      *reinterpret_cast<u16x8_t*>(
-          k_cache + ((pg * Hkv + h) * kPage + row) * D + dg * 8) = v;
-    }
-    // V: e = (h, dg, j), j fastest
-    {
-      const int j = e % n;
-      const int hd = e / n;
-      const int dg = hd % DG;
-      const int h = hd / DG;
-      const int p = c + j;
-      const int64_t pg = bt[p / kPage];
-      const int row = p % kPage;
-      const u16x8_t v = *reinterpret_cast<const u16x8_t*>(
-          v_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h) * D + dg * 8);
-      uint16_t* dst = v_cache + ((pg * Hkv + h) * D + dg * 8) * kPage + row;
+  const int total = n * NH * DG;
+  const int all = total * (l1 - l0);
+  for (int e0 = 0; e0 < all; e0 += kThreads * kAppendBatch) {
+    u16x8_t kv[kAppendBatch], vv[kAppendBatch];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) dst[k * kPage] = v[k];
+    for (int u = 0; u < kAppendBatch; ++u) {
+      const int e2 = e0 + u * kThreads + threadIdx.x;
+      if (e2 >= all) break;
+      const int l = l0 + e2 / total, e = e2 % total;
+      const uint16_t* k_phys = a.k_phys + l * a.win_lstride;
+      const uint16_t* v_phys = a.v_phys + l * a.win_lstride;
+      // K: e = (j, h, dg), dg fastest
+      const int dg = e % DG, jh = e / DG;
+      kv[u] = *reinterpret_cast<const u16x8_t*>(
+          k_phys + ((static_cast<int64_t>(b) * W + jh / NH) * Hkv + h0 +
+                    jh % NH) * D + dg * 8);
+      // V: e = (h, dg, j), j fastest
+      const int j = e % n, hd = e / n;
+      vv[u] = *reinterpret_cast<const u16x8_t*>(
+          v_phys + ((static_cast<int64_t>(b) * W + j) * Hkv + h0 + hd / DG) *
+                       D + (hd % DG) * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < kAppendBatch; ++u) {
+      const int e2 = e0 + u * kThreads + threadIdx.x;
+      if (e2 >= all) break;
+      const int l = l0 + e2 / total, e = e2 % total;
+      uint16_t* k_cache = a.k_cache + l * a.cache_lstride;
+      uint16_t* v_cache = a.v_cache + l * a.cache_lstride;
+      {
+        const int dg = e % DG, jh = e / DG;
+        const int h = h0 + jh % NH, p = c + jh / NH;
+        const int64_t pg = bt[p / kPage];
+        *reinterpret_cast<u16x8_t*>(
+            k_cache + ((pg * Hkv + h) * kPage + p % kPage) * D + dg * 8) = kv[u];
+      }
+      {
+        const int j = e % n, hd = e / n;
+        const int dg = hd % DG, h = h0 + hd / DG, p = c + j;
+        const int64_t pg = bt[p / kPage];
+        uint16_t* dst =
+            v_cache + ((pg * Hkv + h) * D + dg * 8) * kPage + p % kPage;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) dst[k * kPage] = vv[u][k];
+      }
     }
   }
 }
 
-// Extends the caches of layer blockIdx.y of sequence blockIdx.x before
-// commit_kernel updates the window (it reads the same pre-step state and
-// finds the same run).
+// Extends the caches of layer blockIdx.y of sequence blockIdx.x, kv head
+// blockIdx.z, before commit_kernel updates the window (it reads the same
+// pre-step state and finds the same run).
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(CommitArgs a) {
-  const int b = blockIdx.x, l = blockIdx.y;
+  const int b = blockIdx.x, l = blockIdx.y, h = blockIdx.z;
   __shared__ int s_n, s_c;
   if (threadIdx.x < kWave) {
     const Run r = committed_run(a, b);
@@ -171,7 +186,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(CommitArgs a) {
     }
   }
   __syncthreads();
-  if (s_n > 0) append_rows(a, b, s_n, s_c, l, l + 1);
+  if (s_n > 0) append_rows(a, b, s_n, s_c, l, l + 1, h, h + 1);
 }
 
 __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
@@ -248,7 +263,7 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
   __syncthreads();
   if (!s_ok) return;
 
-  if (s_n > 0) append_rows(a, b, s_n, s_c, 0, a.n_layers);
+  if (s_n > 0) append_rows(a, b, s_n, s_c, 0, a.n_layers, 0, a.Hkv);
 }
 
 }  // namespace
@@ -291,12 +306,14 @@ int commit_impl(int32_t* win_tok, int32_t* win_start, const int32_t* argmax,
   a.win_lstride = static_cast<int64_t>(B) * W * Hkv * D;
   a.cache_lstride = num_pages * Hkv * kPage * D;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (n_layers > 1) {
-    // one workgroup per (sequence, layer), before the window changes; the
-    // commit kernel then extends no cache
-    if (n_layers > 65535) return WEDLM_E_SHAPE;
-    hipLaunchKernelGGL(kv_append_kernel, dim3(B, n_layers), dim3(kThreads), 0,
-                       st, a);
+  if (n_layers > 1 || B >= 4) {
+    // one workgroup per (sequence, layer, kv head), before the window
+    // changes; the commit kernel then extends no cache.  (With fewer
+    // sequences and one layer the commit kernel's own workgroup copies the
+    // rows, which saves a launch.)
+    if (n_layers > 65535 || Hkv > 65535) return WEDLM_E_SHAPE;
+    hipLaunchKernelGGL(kv_append_kernel, dim3(B, n_layers, Hkv),
+                       dim3(kThreads), 0, st, a);
     WEDLM_LAUNCH_CHECK();
     a.n_layers = 0;
   }
