@@ -26,9 +26,11 @@
 //   running sum shows that some term exceeded 2^64 (never for scores that
 //   grow by less than 64 log2 units past the first tile; a rare,
 //   wave-uniform branch otherwise).
-// Split-K: the prefix is split so that the grid fills the CUs; partials
-//   (unnormalised O, running max and sum) are merged by a combine kernel.
-//   With a single split the main kernel normalises and writes the output.
+// Split-K: the prefix is split so that the grid fills the CUs; each split
+//   writes its O normalised by its own sum, rounded to bf16 (the precision
+//   of the P operand the MFMAs already take), with its running max and sum
+//   in fp32, and a combine kernel merges them.  With a single split the
+//   main kernel normalises and writes the output.
 // Roofline: the KV stream, 4 * D * Hkv bytes per prefix position, read once
 // per (sequence, kv head, query block); W*G query rows per kv head give an
 // arithmetic intensity of W*G flop/byte (256 at W=64, G=4).
@@ -61,7 +63,7 @@ struct AttnArgs {
   uint16_t* out;          // [B, W, Hq, D]
   float* lse;             // [B, W, Hq] or null
   int32_t* status;        // [B] or null
-  float* ws_o;            // [B, Hkv, rows_pad, nsplit, D]
+  uint16_t* ws_o;         // [B, Hkv, rows_pad, nsplit, D] bf16, normalised
   float2* ws_ml;          // [B, Hkv, rows_pad, nsplit]
   int64_t num_pages;
   int B, W, Hq, Hkv, G, max_pages, max_prefix, nsplit, qblocks,
@@ -124,7 +126,7 @@ Plan make_plan(int B, int W, int Hq, int Hkv, int D, int max_prefix) {
     p.ws_bytes = 0;
   } else {
     const size_t n = static_cast<size_t>(B) * Hkv * p.rows_pad * p.nsplit;
-    p.ws_bytes = n * D * sizeof(float) + 256 + n * sizeof(float2);
+    p.ws_bytes = n * D * sizeof(uint16_t) + 256 + n * sizeof(float2);
   }
   return p;
 }
@@ -810,15 +812,18 @@ tiles_done:
         a.lse[(static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]] =
             (m2[q] + __log2f(l_tot)) * kLn2;
     } else {
-      float* wp = a.ws_o + (rows_base * a.nsplit + split) * D;
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      uint16_t* wp = a.ws_o + (rows_base * a.nsplit + split) * D;
 #pragma unroll
       for (int m = 0; m < NM; ++m)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
           const int d = m * 32 + g4 * 8 + hf * 4;
-          const floatx4_t v = {o[q][m][g4 * 4 + 0], o[q][m][g4 * 4 + 1],
-                               o[q][m][g4 * 4 + 2], o[q][m][g4 * 4 + 3]};
-          *reinterpret_cast<floatx4_t*>(wp + d) = v;
+          const u16x4_t v = {f32_to_bf16(o[q][m][g4 * 4 + 0] * inv),
+                             f32_to_bf16(o[q][m][g4 * 4 + 1] * inv),
+                             f32_to_bf16(o[q][m][g4 * 4 + 2] * inv),
+                             f32_to_bf16(o[q][m][g4 * 4 + 3] * inv)};
+          *reinterpret_cast<u16x4_t*>(wp + d) = v;
         }
       if (hf == 0)
         a.ws_ml[rows_base * a.nsplit + split] =
@@ -827,15 +832,17 @@ tiles_done:
   }
 }
 
-// Merge of the split partials: D/4 threads per (b, kv head, row), each
-// owning four consecutive d, 256 threads per workgroup.  The (m, l) pairs
-// and up to eight partial vectors are loaded before any is used, so one
-// memory round trip covers the row.
+// Merge of the split partials: D/8 threads per (b, kv head, row), each
+// owning eight consecutive d (one 16-byte load per split), 256 threads per
+// workgroup.  O = sum_s 2^(m_s - M) l_s O_s / sum_s 2^(m_s - M) l_s over the
+// splits s of the row (O_s normalised by l_s).  The (m, l) pairs and up to
+// eight partial vectors are loaded before any is used, so one memory round
+// trip covers the row.
 constexpr int kCombineThreads = 256;
 
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs a) {
-  constexpr int TPR = D / 4;                       // threads per row
+  constexpr int TPR = D / 8;                       // threads per row
   constexpr int RPW = kCombineThreads / TPR;       // rows per workgroup
   constexpr int kMaxFast = 8;
   const int rows = a.W * a.G;
@@ -848,18 +855,18 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
   int c;
   if (!seq_ok(a, b, c)) return;
   const int nsplit_b = seq_split(c, a.nsplit).n;
-  const int d = (threadIdx.x % TPR) * 4;
+  const int d = (threadIdx.x % TPR) * 8;
   const int64_t rows_base =
       (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
   const float2* ml = a.ws_ml + rows_base * a.nsplit;
-  const float* op = a.ws_o + rows_base * a.nsplit * D + d;
+  const uint16_t* op = a.ws_o + rows_base * a.nsplit * D + d;
   float2 mls[kMaxFast];
-  floatx4_t vs[kMaxFast];
+  u16x8_t vs[kMaxFast];
 #pragma unroll
   for (int s = 0; s < kMaxFast; ++s) {
     if (s < nsplit_b) {
       mls[s] = ml[s];
-      vs[s] = *reinterpret_cast<const floatx4_t*>(op + static_cast<int64_t>(s) * D);
+      vs[s] = *reinterpret_cast<const u16x8_t*>(op + static_cast<int64_t>(s) * D);
     }
   }
   float M = kNegInf;
@@ -869,30 +876,31 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
   for (int s = kMaxFast; s < nsplit_b; ++s) M = fmaxf(M, ml[s].x);
   const float Mu = (M == kNegInf) ? 0.f : M;
   float L = 0.f;
-  floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < kMaxFast; ++s) {
     if (s < nsplit_b) {
-      const float w = __builtin_amdgcn_exp2f(mls[s].x - Mu);
-      L += w * mls[s].y;
+      const float w = __builtin_amdgcn_exp2f(mls[s].x - Mu) * mls[s].y;
+      L += w;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) acc[k] += w * vs[s][k];
+      for (int k = 0; k < 8; ++k) acc[k] += w * bf16_to_f32(vs[s][k]);
     }
   }
   for (int s = kMaxFast; s < nsplit_b; ++s) {
-    const float w = __builtin_amdgcn_exp2f(ml[s].x - Mu);
-    L += w * ml[s].y;
-    const floatx4_t v = *reinterpret_cast<const floatx4_t*>(op + static_cast<int64_t>(s) * D);
+    const float w = __builtin_amdgcn_exp2f(ml[s].x - Mu) * ml[s].y;
+    L += w;
+    const u16x8_t v = *reinterpret_cast<const u16x8_t*>(op + static_cast<int64_t>(s) * D);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) acc[k] += w * v[k];
+    for (int k = 0; k < 8; ++k) acc[k] += w * bf16_to_f32(v[k]);
   }
   const int qi = r / a.G;
   const int qh = kvh * a.G + r % a.G;
   const int64_t orow = (static_cast<int64_t>(b) * a.W + qi) * a.Hq + qh;
   const float inv = L > 0.f ? 1.f / L : 0.f;
-  const u16x4_t o4 = {f32_to_bf16(acc[0] * inv), f32_to_bf16(acc[1] * inv),
-                      f32_to_bf16(acc[2] * inv), f32_to_bf16(acc[3] * inv)};
-  *reinterpret_cast<u16x4_t*>(a.out + orow * D + d) = o4;
+  u16x8_t o8;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) o8[k] = f32_to_bf16(acc[k] * inv);
+  *reinterpret_cast<u16x8_t*>(a.out + orow * D + d) = o8;
   if (a.lse && d == 0) a.lse[orow] = (M + __log2f(L)) * kLn2;
 }
 
@@ -924,7 +932,7 @@ int launch(const AttnArgs& a, const Plan& p, hipStream_t st) {
   WEDLM_LAUNCH_CHECK();
   if (a.nsplit > 1) {
     const int64_t total_rows = static_cast<int64_t>(a.B) * a.Hkv * a.W * a.G;
-    constexpr int rpw = kCombineThreads / (D / 4);
+    constexpr int rpw = kCombineThreads / (D / 8);
     hipLaunchKernelGGL((attn_combine_kernel<D>),
                        dim3(static_cast<unsigned>((total_rows + rpw - 1) / rpw)),
                        dim3(kCombineThreads), 0, st, a);
@@ -981,8 +989,8 @@ int window_attn_impl(
   if (p.nsplit > 1) {
     const size_t n = static_cast<size_t>(B) * Hkv * p.rows_pad * p.nsplit;
     char* base = static_cast<char*>(workspace);
-    a.ws_o = reinterpret_cast<float*>(base);
-    size_t off = (n * D * sizeof(float) + 255) & ~static_cast<size_t>(255);
+    a.ws_o = reinterpret_cast<uint16_t*>(base);
+    size_t off = (n * D * sizeof(uint16_t) + 255) & ~static_cast<size_t>(255);
     a.ws_ml = reinterpret_cast<float2*>(base + off);
   }
   return D == 128 ? launch<128>(a, p, st) : launch<64>(a, p, st);
