@@ -4,6 +4,10 @@
 // produces the logits the mask slots are scored on).  The fp32 logits are
 // never written to memory.
 //
+// Up to 32 rows with Hd = 2048 or 4096 take lm_head_ks_kernel (the k split
+// over the waves of a workgroup, described above it); every other shape the
+// kernel below.
+//
 // Work decomposition (persistent, balanced):
 //   grid      = n_rg row groups x n_slot slots, sized from the occupancy so
 //               that every workgroup is resident at once
@@ -38,6 +42,8 @@
 //   the slots in a merge kernel over a workspace of per-slot states.
 // Roofline: 2 * R * Hd * V flops against V * Hd * 2 weight bytes per row
 //   group; R rows in one group give an intensity of R flop/byte.
+#include <algorithm>
+
 #include "common.h"
 #include "score_state.h"
 
@@ -292,6 +298,164 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   }
 }
 
+// Few rows (R <= 32): the k split over the waves.  A workgroup of NWV
+// waves owns a contiguous run of 32-row vocabulary blocks (the runs of the
+// grid differ by at most one block); wave w owns the k steps w, w + NWV,
+// w + 2 NWV, ... of every block, so at any time the workgroup reads NWV
+// neighbouring 128-byte pieces of each of the block's 32 rows.  The wave's
+// hidden-row fragments of its k steps stay in registers for the whole run
+// (SPW steps x 4 MFMAs); its weight rows go through a private
+// double-buffered 4 KB LDS tile per k step (loaded coalesced, eight full
+// 128-byte rows per instruction, PF steps ahead across block boundaries),
+// so the loop needs no barrier.  After each block the NWV partial 32 x 32
+// logit tiles are summed through LDS in wave order (one barrier; two
+// buffers alternate between blocks) and wave w scores 16 / NWV of the 16
+// vocabulary rows each lane holds.
+// Measured at Hd 4096, V 151936 (R = 16 and 32): 207 us, 6.0 TB/s, where
+// the vocabulary split over 2048 wave streams (74 rows each) took 236-245
+// us; with four waves and a contiguous k range per wave (each reading 2 KB
+// apart in every row) the k split took 285 us, and more vocabulary streams
+// made the other kernel slower, not faster: the number of scattered
+// streams in flight, not padding, set its rate.
+constexpr int kKsWaves = 8;
+constexpr int kKsPF = 4;   // register stages of weight steps in flight
+
+template <int SPW, int PF>
+__global__ __launch_bounds__(kKsWaves * kWave) void lm_head_ks_kernel(LmArgs a) {
+  constexpr int NWV = kKsWaves;
+  constexpr int EPW = 16 / NWV;                            // entries per wave
+  static_assert(SPW % PF == 0 && (SPW & 1) == 0, "stages line up with blocks");
+  static_assert(EPW == 2 || EPW == 4, "waves");
+  constexpr int kWTile = 32 * kKStep * 2;                  // 4 KB
+  constexpr int kRedBuf = NWV * 16 * kWave * 4;
+  __shared__ __attribute__((aligned(16))) char smem[NWV * 2 * kWTile + 2 * kRedBuf];
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  const int col = lane & 31;
+  const int hf = lane >> 5;
+  const int g = blockIdx.x;
+  const int nba = (a.V + 31) / 32;
+  const int bb0 = static_cast<int>(static_cast<int64_t>(g) * nba / a.n_slot);
+  const int bb1 = static_cast<int>(static_cast<int64_t>(g + 1) * nba / a.n_slot);
+  const int nblk = bb1 - bb0;
+  const int total = nblk * SPW;
+
+  // hidden-row fragments of this wave's k steps (rows past R re-read R-1)
+  const uint16_t* hrow =
+      a.hidden + static_cast<int64_t>(min(col, a.R - 1)) * a.Hd + hf * 32;
+  bf16x8_t bfr[SPW][4];
+#pragma unroll
+  for (int s = 0; s < SPW; ++s)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      bfr[s][j] = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const u16x8_t*>(
+                        hrow + (s * NWV + wave) * kKStep + j * 8));
+
+  // weights: 32 rows x 128 bytes of a k step as four 1 KB loads (lane l:
+  // row l/8 + 8i, chunk l%8); rows past V re-read row V-1 (masked later),
+  // steps past the run re-read its last step
+  const int w_row = lane >> 3, w_chunk = lane & 7;
+  char* const wtile = smem + wave * 2 * kWTile;
+  auto wload = [&](int q, u16x8_t (&r)[4]) {
+    q = min(q, total - 1);
+    const int bi = q / SPW;
+    const int s = q - bi * SPW;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = min((bb0 + bi) * 32 + w_row + 8 * i, a.V - 1);
+      r[i] = __builtin_nontemporal_load(reinterpret_cast<const u16x8_t*>(
+          a.w + static_cast<int64_t>(v) * a.Hd + (s * NWV + wave) * kKStep +
+          w_chunk * 8));
+    }
+  };
+  auto wstore = [&](char* wb, const u16x8_t (&r)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<u16x8_t*>(wb + h_off(w_row + 8 * i, w_chunk)) = r[i];
+  };
+
+  floatx16_t acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+  State st = empty_state();
+  const ExpScale sc = exp_scale(a.c2);
+  float* const red = reinterpret_cast<float*>(smem + NWV * 2 * kWTile);
+
+  u16x8_t wa[PF][4];
+  if (nblk > 0) {
+    wload(0, wa[0]);
+    wstore(wtile, wa[0]);
+#pragma unroll
+    for (int p = 0; p < PF; ++p) wload(p + 1, wa[(p + 1) % PF]);
+  }
+  for (int bi = 0; bi < nblk; ++bi) {
+#pragma unroll
+    for (int s = 0; s < SPW; ++s) {
+      const int q = bi * SPW + s;
+      const int u = s % PF;                                // = q % PF
+      const char* wb = wtile + (s & 1) * kWTile;           // SPW is even
+      bf16x8_t afr[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+        afr[kk] = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u16x8_t*>(wb + h_off(col, hf * 4 + kk)));
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(afr[kk], bfr[s][kk], acc,
+                                                       0, 0, 0);
+      wstore(wtile + ((s + 1) & 1) * kWTile, wa[(u + 1) % PF]);
+      wload(q + 1 + PF, wa[(u + 1) % PF]);
+    }
+    // partial tiles -> LDS [buffer][wave][e/4][lane] (16 bytes per entry)
+    float* rb = red + (bi & 1) * (kRedBuf / 4);
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4) {
+      const floatx4_t v = {acc[4 * e4], acc[4 * e4 + 1], acc[4 * e4 + 2],
+                           acc[4 * e4 + 3]};
+      *reinterpret_cast<floatx4_t*>(rb + ((wave * 4 + e4) * kWave + lane) * 4) = v;
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+    __syncthreads();
+    // wave w: entries e = EPW*w .. EPW*w + EPW-1, summed over the waves in
+    // order; entry e of lane (col, hf) is vocabulary row 8(e/4) + 4hf + e%4
+    const int e0 = wave * EPW;
+    float sum[EPW];
+#pragma unroll
+    for (int t = 0; t < EPW; ++t) sum[t] = 0.f;
+#pragma unroll
+    for (int w2 = 0; w2 < NWV; ++w2) {
+      const float* src = rb + ((w2 * 4 + e0 / 4) * kWave + lane) * 4 + e0 % 4;
+#pragma unroll
+      for (int t = 0; t < EPW; ++t) sum[t] += src[t];
+    }
+    const int v0 = (bb0 + bi) * 32 + 8 * (e0 / 4) + 4 * hf + e0 % 4;
+    float x[EPW];
+    int idx[EPW];
+#pragma unroll
+    for (int t = 0; t < EPW; ++t) {
+      idx[t] = v0 + t;
+      x[t] = v0 + t < a.V ? sum[t] : kNegInf;
+    }
+    push_block(st, x, idx, sc);
+  }
+
+  // merge: the two lane halves, then the waves (LDS, after a barrier)
+  merge(st, shfl_xor_state(st, 32), a.c2);
+  __syncthreads();
+  State* sred = reinterpret_cast<State*>(red);            // [wave][32]
+  if (hf == 0) sred[wave * 32 + col] = st;
+  __syncthreads();
+  if (threadIdx.x < 32 && threadIdx.x < a.R) {
+    const int r = threadIdx.x;
+    State m = sred[r];
+    for (int w2 = 1; w2 < NWV; ++w2) merge(m, sred[w2 * 32 + r], a.c2);
+    if (a.n_slot == 1) finish(m, r, a.argmax, a.entropy, a.pmax);
+    else a.ws[static_cast<int64_t>(r) * a.n_slot + g] = m;
+  }
+}
+
 // Merge the slot states of each row, lanes over slots.
 __global__ __launch_bounds__(kWave) void lm_head_merge_kernel(LmArgs a) {
   const int row = blockIdx.x;
@@ -347,13 +511,32 @@ int shape_index(Shape s) { return s.rw == 1 ? s.nb - 1 : 4; }
 struct LmPlan {
   Shape sh;
   int n_rg, n_slot, nblk;
+  int ks_spw;   // > 0: the k-split kernel with this many k steps per wave
 };
+
+// The k-split kernel takes R <= 32 rows and Hd = 2048 or 4096 (k steps per
+// wave a compile-time count).
+int ks_steps_per_wave(int R, int Hd) {
+  if (R > 32 || Hd % (kKStep * kKsWaves) != 0) return 0;
+  const int spw = Hd / kKStep / kKsWaves;
+  return spw == 4 || spw == 8 ? spw : 0;
+}
+
+template <int SPW>
+int ks_resident_per_cu() {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &n, reinterpret_cast<const void*>(lm_head_ks_kernel<SPW, kKsPF>),
+          kKsWaves * kWave, 0) != hipSuccess || n < 1)
+    n = 1;
+  return n;
+}
 
 bool lm_plan(int R, int Hd, int V, LmPlan* p) {
   if (!lm_shape_ok(R, Hd, V)) return false;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
-  static int cus[64], occ[64][kShapes];
+  static int cus[64], occ[64][kShapes], occ_ks[64][2];
   if (cus[dev] == 0) {
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount,
@@ -364,7 +547,19 @@ bool lm_plan(int R, int Hd, int V, LmPlan* p) {
     occ[dev][2] = resident_per_cu<3, 1, 2>();
     occ[dev][3] = resident_per_cu<4, 1, 2>();
     occ[dev][4] = resident_per_cu<4, 2, 2>();
+    occ_ks[dev][0] = ks_resident_per_cu<4>();
+    occ_ks[dev][1] = ks_resident_per_cu<8>();
     cus[dev] = n;
+  }
+  p->ks_spw = ks_steps_per_wave(R, Hd);
+  if (p->ks_spw > 0) {
+    const int oi = p->ks_spw == 4 ? 0 : 1;
+    const int nba = (V + 31) / 32;
+    p->sh = Shape{1, 1};
+    p->n_rg = 1;
+    p->n_slot = std::min(cus[dev] * occ_ks[dev][oi], nba);
+    p->nblk = 0;
+    return true;
   }
   p->sh = group_shape(R);
   const int rg = 32 * p->sh.nb * p->sh.rw;
@@ -431,15 +626,24 @@ extern "C" int wedlm_lm_head_score(const uint16_t* hidden,
   // row group covers every slot
   const int64_t grid = 8ll * p.n_rg * ((p.n_slot + 7) / 8);
   if (grid > (1ll << 30)) return WEDLM_E_SHAPE;
-  const bool nt = p.n_rg == 1;
-  switch (shape_index(p.sh)) {
-    case 0: launch<1, 1, kPF>(nt, grid, st, a); break;
-    case 1: launch<2, 1, kPF>(nt, grid, st, a); break;
-    case 2: launch<3, 1, 2>(nt, grid, st, a); break;
-    case 3: launch<4, 1, 2>(nt, grid, st, a); break;
-    default: launch<4, 2, 2>(nt, grid, st, a); break;
+  if (p.ks_spw > 0) {
+    const dim3 g(p.n_slot), b(kKsWaves * kWave);
+    if (p.ks_spw == 4)
+      hipLaunchKernelGGL((lm_head_ks_kernel<4, kKsPF>), g, b, 0, st, a);
+    else
+      hipLaunchKernelGGL((lm_head_ks_kernel<8, kKsPF>), g, b, 0, st, a);
+    WEDLM_LAUNCH_CHECK();
+  } else {
+    const bool nt = p.n_rg == 1;
+    switch (shape_index(p.sh)) {
+      case 0: launch<1, 1, kPF>(nt, grid, st, a); break;
+      case 1: launch<2, 1, kPF>(nt, grid, st, a); break;
+      case 2: launch<3, 1, 2>(nt, grid, st, a); break;
+      case 3: launch<4, 1, 2>(nt, grid, st, a); break;
+      default: launch<4, 2, 2>(nt, grid, st, a); break;
+    }
+    WEDLM_LAUNCH_CHECK();
   }
-  WEDLM_LAUNCH_CHECK();
   if (p.n_slot > 1) {
     hipLaunchKernelGGL(lm_head_merge_kernel, dim3(R), dim3(kWave), 0, st, a);
     WEDLM_LAUNCH_CHECK();

@@ -132,12 +132,45 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
 // one item = 8 rotation pairs of one head (two 16-byte loads), the D/16
 // items of a head sit on consecutive lanes and reduce their sum of squares
 // with xor shuffles.
+// PART: the q|k|v row comes as the n_ks fp32 partials of a split product
+// ([n_ks, M, H*D]); they are added in split order and rounded to bf16 (the
+// product's own output precision) on the way in.
 // ---------------------------------------------------------------------------
 constexpr int kQkThreads = 256;
 constexpr int kMaxHalf = 64;
 
+template <bool PART>
+__device__ __forceinline__ u16x8_t qkv_load8(const uint16_t* x,
+                                             const float* part, int64_t pstride,
+                                             int n_ks, int64_t off) {
+  if constexpr (!PART) {
+    return *reinterpret_cast<const u16x8_t*>(x + off);
+  } else {
+    floatx4_t lo = *reinterpret_cast<const floatx4_t*>(part + off);
+    floatx4_t hi = *reinterpret_cast<const floatx4_t*>(part + off + 4);
+    for (int k = 1; k < n_ks; ++k) {
+      const floatx4_t a = *reinterpret_cast<const floatx4_t*>(part + k * pstride + off);
+      const floatx4_t b = *reinterpret_cast<const floatx4_t*>(part + k * pstride + off + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lo[e] += a[e];
+        hi[e] += b[e];
+      }
+    }
+    u16x8_t r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      r[e] = f32_to_bf16(lo[e]);
+      r[e + 4] = f32_to_bf16(hi[e]);
+    }
+    return r;
+  }
+}
+
+template <bool PART>
 __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
-    const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ gq,
+    const uint16_t* __restrict__ qkv, const float* __restrict__ part,
+    int n_ks, int M, const uint16_t* __restrict__ gq,
     const uint16_t* __restrict__ gk, const int32_t* __restrict__ pos_ids,
     int Hq, int Hkv, int D, double theta, float eps,
     uint16_t* __restrict__ q_out, uint16_t* __restrict__ k_out,
@@ -147,7 +180,8 @@ __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
   const int per_head = half / 8;                  // items of a head: 4 or 8
   const int n_items = (Hq + Hkv) * per_head;
   const int H = Hq + 2 * Hkv;
-  const uint16_t* x = qkv + static_cast<int64_t>(t) * H * D;
+  const int64_t row = static_cast<int64_t>(t) * H * D;   // element offset
+  const int64_t pstride = static_cast<int64_t>(M) * H * D;
   __shared__ double s_cos[kMaxHalf], s_sin[kMaxHalf];
   if (threadIdx.x < half) {
     const int j = threadIdx.x;
@@ -168,8 +202,8 @@ __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
     const int j0 = live ? (it - head * per_head) * 8 : 0;
     u16x8_t lo8 = {}, hi8 = {};
     if (live) {
-      lo8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0);
-      hi8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0 + half);
+      lo8 = qkv_load8<PART>(qkv, part, pstride, n_ks, row + head * D + j0);
+      hi8 = qkv_load8<PART>(qkv, part, pstride, n_ks, row + head * D + j0 + half);
     }
     float a[8], b[8], ss = 0.f;
 #pragma unroll
@@ -197,10 +231,10 @@ __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
     *reinterpret_cast<u16x8_t*>(dst + j0) = olo;
     *reinterpret_cast<u16x8_t*>(dst + j0 + half) = ohi;
   }
-  const u16x8_t* xv = reinterpret_cast<const u16x8_t*>(x + (Hq + Hkv) * D);
   u16x8_t* dv =
       reinterpret_cast<u16x8_t*>(v_out + static_cast<int64_t>(t) * Hkv * D);
-  for (int e = threadIdx.x; e < Hkv * D / 8; e += kQkThreads) dv[e] = xv[e];
+  for (int e = threadIdx.x; e < Hkv * D / 8; e += kQkThreads)
+    dv[e] = qkv_load8<PART>(qkv, part, pstride, n_ks, row + (Hq + Hkv) * D + e * 8);
 }
 
 // ---------------------------------------------------------------------------
@@ -700,11 +734,12 @@ bool gemm_shape_ok(int M, int N, int K) {
 size_t up256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
 // The plan of one product: row block, row groups and K splits.  A residual-
-// add product (N = hidden: few feature blocks) splits K over workgroups
-// until about one workgroup per CU streams weights, never below one step
-// per wave; the splits write fp32 partials ([n_ks, M, N]) that the next
-// RMSNorm (or, standing alone, add_partials_kernel) sums into the residual
-// stream in split order.  No workgroup waits for another.
+// add product (N = hidden: few feature blocks), and the q|k|v product when
+// its caller sums the partials (split_store), split K over workgroups until
+// about one workgroup per CU streams weights, never below one step per wave;
+// the splits write fp32 partials ([n_ks, M, N]) that the next RMSNorm (or,
+// standing alone, add_partials_kernel), or the q/k norm, sums in split
+// order.  No workgroup waits for another.
 struct GemmPlan {
   int nb, n_nb, n_rg, n_ks;
   bool two_d;             // the 2-D tiled kernel (packed activations, many rows)
@@ -717,9 +752,12 @@ struct GemmPlan {
 // step)
 constexpr int k2dMinRows = 256;
 
+// workgroups a split product aims at: about one per CU (with few rows, 512
+// and 768 made the 36-layer step at B = 1 slower: 5.00 -> 5.29 and 5.91 ms)
 constexpr int kGemmTargetWgs = 256;
 
-GemmPlan gemm_plan(int M, int N, int K, int epi, bool xp = false) {
+GemmPlan gemm_plan(int M, int N, int K, int epi, bool xp = false,
+                   bool split_store = false) {
   GemmPlan p{};
   if (xp && M >= k2dMinRows) {
     // 2-D tiles; a residual-add product with few tiles splits K (at least
@@ -742,7 +780,7 @@ GemmPlan gemm_plan(int M, int N, int K, int epi, bool xp = false) {
   p.n_nb = N / 32;
   p.n_rg = (M + 32 * p.nb - 1) / (32 * p.nb);
   p.n_ks = 1;
-  if (epi == kAddF32) {
+  if (epi == kAddF32 || (epi == kStoreBf16 && split_store)) {
     const int wgs = p.n_nb * p.n_rg;
     p.n_ks = std::max(1, std::min(kGemmTargetWgs / wgs, K / kKStep / kGWaves));
   }
@@ -760,7 +798,7 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
   if (!x || !w || !out) return WEDLM_E_ARG;
   if (epi != kStoreBf16 && epi != kAddF32 && epi != kSwiglu) return WEDLM_E_ARG;
   if (!gemm_shape_ok(M, N, K) || ldo < N) return WEDLM_E_SHAPE;
-  const GemmPlan p = gemm_plan(M, N, K, epi, xp);
+  const GemmPlan p = gemm_plan(M, N, K, epi, xp, defer);
   if (p.part_bytes > 0 && (!part || part_bytes < p.part_bytes))
     return WEDLM_E_WORKSPACE;
   if (p.two_d) {
@@ -782,7 +820,7 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
                          dim3(kGThreads), 0, st, g);
     WEDLM_LAUNCH_CHECK();
     if (n_ks_out) *n_ks_out = p.n_ks;
-    if (p.n_ks > 1 && epi == kStoreBf16) {
+    if (p.n_ks > 1 && epi == kStoreBf16 && !defer) {
       const int64_t total4 = static_cast<int64_t>(M) * (N / 4);
       hipLaunchKernelGGL(sum_partials_bf16_kernel, dim3((total4 + 255) / 256),
                          dim3(256), 0, st, static_cast<uint16_t*>(out), ldo,
@@ -844,6 +882,25 @@ int norm(float* x, const float* part, int n_ks, int M, int Hd,
   return WEDLM_OK;
 }
 
+// q/k RMSNorm + RoPE of M rows; part: the n_ks > 1 split partials of the
+// q|k|v product instead of its bf16 output
+int qk_norm_rope(const uint16_t* qkv, const float* part, int n_ks, int M,
+                 const uint16_t* gq, const uint16_t* gk, const int32_t* pos,
+                 int Hq, int Hkv, int D, double theta, float eps,
+                 uint16_t* q_out, uint16_t* k_out, uint16_t* v_out,
+                 hipStream_t st) {
+  if (part && n_ks > 1)
+    hipLaunchKernelGGL(qk_norm_rope_kernel<true>, dim3(M), dim3(kQkThreads), 0,
+                       st, qkv, part, n_ks, M, gq, gk, pos, Hq, Hkv, D, theta,
+                       eps, q_out, k_out, v_out);
+  else
+    hipLaunchKernelGGL(qk_norm_rope_kernel<false>, dim3(M), dim3(kQkThreads), 0,
+                       st, qkv, part, 1, M, gq, gk, pos, Hq, Hkv, D, theta,
+                       eps, q_out, k_out, v_out);
+  WEDLM_LAUNCH_CHECK();
+  return WEDLM_OK;
+}
+
 bool config_ok(const wedlm_model_config* c) {
   return c && c->n_layers >= 1 && c->hidden >= 256 && c->hidden % 256 == 0 &&
          c->n_kv_heads >= 1 && c->n_heads % c->n_kv_heads == 0 &&
@@ -870,13 +927,13 @@ Carve carve(const wedlm_model_config* c, int B, int W, int max_prefix_len) {
   // next RMSNorm before the other is written)
   const int Mi = static_cast<int>(M);
   const bool big = Mi >= k2dMinRows;   // o's input packed (2-D kernel)
-  // and of the q|k|v product (summed right after it)
+  // and of the q|k|v product (summed by the q/k norm that reads it)
   k.part_bytes = std::max(
       std::max(gemm_plan(Mi, c->hidden, c->n_heads * c->head_dim, kAddF32, big)
                    .part_bytes,
                gemm_plan(Mi, c->hidden, c->inter, kAddF32, true).part_bytes),
       gemm_plan(Mi, (c->n_heads + 2 * c->n_kv_heads) * c->head_dim, c->hidden,
-                kStoreBf16, true).part_bytes);
+                kStoreBf16, true, true).part_bytes);
   k.part = off; off += up256(k.part_bytes);
   k.x = off;    off += up256(M * Hd * 4);
   const size_t Mp = (M + 31) / 32 * 32;           // packed: whole tiles
@@ -970,12 +1027,9 @@ extern "C" int wedlm_qk_norm_rope(const uint16_t* qkv, const uint16_t* q_gain,
     return WEDLM_E_ARG;
   if (!(rope_theta > 1.0) || !(eps > 0.f)) return WEDLM_E_ARG;
   if (M < 1 || Hq < 1 || Hkv < 1 || (D != 64 && D != 128)) return WEDLM_E_SHAPE;
-  hipLaunchKernelGGL(qk_norm_rope_kernel, dim3(M), dim3(kQkThreads), 0,
-                     static_cast<hipStream_t>(stream), qkv, q_gain, k_gain,
-                     pos_ids, Hq, Hkv, D, rope_theta, eps, q_out, k_out,
-                     v_out);
-  WEDLM_LAUNCH_CHECK();
-  return WEDLM_OK;
+  return qk_norm_rope(qkv, nullptr, 1, M, q_gain, k_gain, pos_ids, Hq, Hkv, D,
+                      rope_theta, eps, q_out, k_out, v_out,
+                      static_cast<hipStream_t>(stream));
 }
 
 extern "C" size_t wedlm_model_workspace_size(const wedlm_model_config* cfg,
@@ -1053,12 +1107,16 @@ extern "C" int wedlm_model_forward(
     WEDLM_TRY(norm(x, part, pend, M, Hd,
                    wt->attn_norm + static_cast<int64_t>(l) * Hd, cfg->rms_eps,
                    xn, true, st));
+    // a split q|k|v product leaves fp32 partials, summed by the q/k norm
+    int qkv_ks = 1;
     WEDLM_TRY(gemm(xn, wt->w_qkv + static_cast<int64_t>(l) * QKV * Hd, M, QKV,
-                   Hd, qkv, QKV, kStoreBf16, part, part_bytes, true, true, st));
-    WEDLM_TRY(wedlm_qk_norm_rope(qkv, wt->q_norm + static_cast<int64_t>(l) * D,
-                                 wt->k_norm + static_cast<int64_t>(l) * D,
-                                 pos_ids, M, Hq, Hkv, D, cfg->rope_theta,
-                                 cfg->rms_eps, q, kl, vl, stream));
+                   Hd, qkv, QKV, kStoreBf16, part, part_bytes, true, true, st,
+                   &qkv_ks));
+    WEDLM_TRY(qk_norm_rope(qkv, part, qkv_ks, M,
+                           wt->q_norm + static_cast<int64_t>(l) * D,
+                           wt->k_norm + static_cast<int64_t>(l) * D, pos_ids,
+                           Hq, Hkv, D, cfg->rope_theta, cfg->rms_eps, q, kl,
+                           vl, st));
     WEDLM_TRY(wedlm_window_attn(
         q, kl, vl, k_cache + l * cache_stride, v_cache + l * cache_stride,
         num_pages, block_table, max_pages, win_start, B, W, Hq, Hkv, D,

@@ -63,6 +63,11 @@ EXACT = [
     (300, 512, 2000),    # two 256-row groups, the second ragged
     (800, 256, 777),     # seven 128-row groups, the last ragged
     (17, 1024, 40000),   # several 32-row blocks per stream
+    # k split over the waves (R <= 32, Hd 2048 / 4096)
+    (7, 2048, 33),       # two blocks, the second with one row
+    (1, 4096, 100),      # fewer blocks than workgroups
+    (16, 2048, 20000),   # four k steps per wave, runs of two or three blocks
+    (32, 4096, 9001),    # eight k steps per wave, ragged last block
 ]
 
 
@@ -81,12 +86,14 @@ def test_lm_head_exact(R, Hd, V, T):
            f"{(err / np.maximum(np.abs(H), 1e-300)).max():.2e}")
 
 
-def test_lm_head_qwen3_shape_sampled():
-    R, Hd, V, T = 384, 4096, 151936, 0.1
+@pytest.mark.parametrize("R", [16, 32, 384])
+def test_lm_head_qwen3_shape_sampled(R):
+    Hd, V, T = 4096, 151936, 0.1
     PL.log(f"case lm_head normal R={R} Hd={Hd} V={V} (sampled rows)")
     hb, wb = WL.lm_head_inputs(R, Hd, V, seed=11)
     gt, gH, gp = _run(hb, wb, T)
-    rows = [0, 1, 63, 127, 128, 200, 255, 256, 383]
+    rows = sorted({r for r in (0, 1, 15, 31, 63, 127, 128, 200, 255, 256, 383)
+                   if r < R})
     tok, H, pm = O.lm_head_score(hb, wb, T, rows=rows)
     # logit error bound per row: Hd * 2^-24 * max_v sum_k |h_k w_vk|
     h = np.abs(O.bf16_to_f64(hb[rows]))
