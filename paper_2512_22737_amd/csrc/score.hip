@@ -18,8 +18,16 @@
 // the terms of a row, and v_exp_f32 gives 2^y.  Only the rescaling of a
 // state to a new maximum evaluates its exponent in fp64.
 //
-// Roofline: 4*V bytes per masked row, read once; grid = masked rows x
-// vocabulary chunks, chunks sized so that every CU has work.
+// Roofline: 4*V bytes per masked row, read once.
+// Work: with 768 rows or more, one workgroup per row (observed rows exit)
+// and no partials.  With fewer rows the chunking follows the rows that are
+// masked in this call, known only on the device: every workgroup counts
+// them (Mt, from n_obs), splits each into nch = ceil(768 / Mt) vocabulary
+// chunks of at least 16K logits, and takes item g = (masked row g / nch,
+// chunk g % nch) of the compacted list, so about 768 workgroups stream
+// whatever the share of observed rows; a merge kernel combines the chunks.
+#include <algorithm>
+
 #include "common.h"
 #include "score_state.h"
 
@@ -124,29 +132,127 @@ struct ScoreArgs {
   const float* logits;
   int64_t row_stride;
   const int32_t* n_obs;
-  int B, W, V, nchunk, chunk;  // chunk: elements per chunk (multiple of 4)
+  int B, W, V;
+  int dyn;                     // chunks from the masked rows (fewer than 1024 rows)
+  int max_nchunk;              // dyn: chunks per row at most (>= 8K logits each)
   double c2;
   int32_t* argmax;
   float* entropy;
   float* pmax;
-  State* ws;                   // [B*W, nchunk] partials (nchunk > 1)
+  State* ws;                   // dyn: [B*W, max_nchunk] partials by masked row
 };
+
+// About three workgroups per CU, chunks of at least 16K logits: 1152
+// workgroups at 384 masked rows and 8K chunks at 16 rows measured 9% and
+// 7% slower.
+constexpr int kTargetWgs = 768;
+constexpr int kMinChunk = 16384;          // logits per chunk at least
+
+__device__ __forceinline__ int clamp_obs(const ScoreArgs& a, int b) {
+  const int no = a.n_obs[b];
+  return no < 0 ? 0 : (no > a.W ? a.W : no);
+}
+
+// The masked rows of the call: sequences in order, rows in order within a
+// sequence.  The first 64 sequences' counts and their inclusive prefix sums
+// are kept in registers (one lane each), so with up to 64 sequences n_obs
+// is read once; further groups of 64 are re-read on demand.
+struct MaskedRows {
+  int no0, c0, inc0;   // this lane's sequence of the first group
+  int total;           // masked rows over all sequences (wave-uniform)
+};
+
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int t = __shfl_up(v, off);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+__device__ MaskedRows masked_rows(const ScoreArgs& a) {
+  MaskedRows m;
+  const int lane = lane_id();
+  m.no0 = lane < a.B ? clamp_obs(a, lane) : a.W;
+  m.c0 = a.W - m.no0;
+  m.inc0 = wave_incl_scan(m.c0);
+  m.total = __shfl(m.inc0, kWave - 1);
+  for (int b0 = kWave; b0 < a.B; b0 += kWave) {
+    const int b = b0 + lane;
+    int c = b < a.B ? a.W - clamp_obs(a, b) : 0;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off);
+    m.total += c;
+  }
+  return m;
+}
+
+// The r-th masked row (0 <= r < total; r wave-uniform) as (b, i).
+__device__ void masked_row(const ScoreArgs& a, const MaskedRows& m, int r,
+                           int& b_out, int& i_out) {
+  int base = 0, no = m.no0, c = m.c0, inc = m.inc0;
+  for (int b0 = 0; b0 < a.B; b0 += kWave) {
+    if (b0 > 0) {
+      const int b = b0 + lane_id();
+      no = b < a.B ? clamp_obs(a, b) : a.W;
+      c = a.W - no;
+      inc = wave_incl_scan(c);
+    }
+    const int tot = __shfl(inc, kWave - 1);
+    if (r < base + tot) {
+      const uint64_t hit = ballot(base + inc > r);
+      const int L = __ffsll(static_cast<unsigned long long>(hit)) - 1;
+      const int excl = __shfl(inc - c, L);
+      b_out = b0 + L;
+      i_out = __shfl(no, L) + (r - base - excl);
+      return;
+    }
+    base += tot;
+  }
+  b_out = 0;
+  i_out = 0;
+}
+
+// Chunks per masked row and their length, from the masked-row count.
+struct ChunkPlan {
+  int nch, chunk;
+};
+__device__ __forceinline__ ChunkPlan chunk_plan(const ScoreArgs& a, int mt) {
+  int n = (kTargetWgs + mt - 1) / mt;
+  n = n > a.max_nchunk ? a.max_nchunk : n;
+  n = n < 1 ? 1 : n;
+  ChunkPlan p;
+  p.chunk = (((a.V + n - 1) / n) + 3) & ~3;
+  p.nch = (a.V + p.chunk - 1) / p.chunk;
+  return p;
+}
 
 // kVec: rows start on 16-byte boundaries (row_stride % 4 == 0 and an
 // aligned base), so the body streams 16-byte loads; otherwise 4-byte loads.
 // Thread t takes float4 groups t, t+256, ... of the chunk, four at a time.
 template <bool kVec>
 __global__ __launch_bounds__(kThreads) void score_kernel(ScoreArgs a) {
-  const int ch = blockIdx.x % a.nchunk;
-  const int row = blockIdx.x / a.nchunk;
-  const int b = row / a.W;
-  const int i = row - b * a.W;
-  int no = a.n_obs[b];
-  no = no < 0 ? 0 : (no > a.W ? a.W : no);
-  if (i < no) return;
+  int row, ch = 0, v0 = 0, v1 = a.V, r = 0, nch = 1;
+  if (a.dyn) {
+    const MaskedRows mr = masked_rows(a);
+    const ChunkPlan cp = chunk_plan(a, mr.total);
+    nch = cp.nch;
+    if (static_cast<int>(blockIdx.x) >= mr.total * nch) return;
+    r = blockIdx.x / nch;
+    ch = blockIdx.x - r * nch;
+    int b, i;
+    masked_row(a, mr, r, b, i);
+    row = b * a.W + i;
+    v0 = ch * cp.chunk;
+    v1 = min(a.V, v0 + cp.chunk);
+  } else {
+    row = blockIdx.x;
+    const int b = row / a.W;
+    if (row - b * a.W < clamp_obs(a, b)) return;
+  }
   const float* x = a.logits + static_cast<int64_t>(row) * a.row_stride;
-  const int v0 = ch * a.chunk;
-  const int v1 = min(a.V, v0 + a.chunk);
   State st = empty_state();
   const ExpScale sc = exp_scale(a.c2);
   constexpr int kStep = kThreads * kBlk;       // logits per workgroup step
@@ -203,50 +309,41 @@ __global__ __launch_bounds__(kThreads) void score_kernel(ScoreArgs a) {
   }
   st = block_reduce(st, a.c2);
   if (threadIdx.x != 0) return;
-  if (a.nchunk == 1) finish(st, row, a.argmax, a.entropy, a.pmax);
-  else a.ws[static_cast<int64_t>(row) * a.nchunk + ch] = st;
+  if (!a.dyn) finish(st, row, a.argmax, a.entropy, a.pmax);
+  else a.ws[static_cast<int64_t>(r) * a.max_nchunk + ch] = st;
 }
 
-// Merge the chunk partials of each masked row, in chunk order.
+// Merge the chunk partials of each masked row, in chunk order (dyn only;
+// workgroup g takes masked row g).
 __global__ __launch_bounds__(kWave) void score_merge_kernel(ScoreArgs a) {
-  const int row = blockIdx.x;
-  const int b = row / a.W;
-  const int i = row - b * a.W;
-  int no = a.n_obs[b];
-  no = no < 0 ? 0 : (no > a.W ? a.W : no);
-  if (i < no) return;
+  const MaskedRows mr = masked_rows(a);
+  const int r = blockIdx.x;
+  if (r >= mr.total) return;
+  const int nch = chunk_plan(a, mr.total).nch;
+  int b, i;
+  masked_row(a, mr, r, b, i);
   State st = empty_state();
-  const State* p = a.ws + static_cast<int64_t>(row) * a.nchunk;
-  for (int c = lane_id(); c < a.nchunk; c += kWave) merge(st, p[c], a.c2);
+  const State* p = a.ws + static_cast<int64_t>(r) * a.max_nchunk;
+  for (int c = lane_id(); c < nch; c += kWave) merge(st, p[c], a.c2);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) merge(st, shfl_xor_state(st, off), a.c2);
-  if (lane_id() == 0) finish(st, row, a.argmax, a.entropy, a.pmax);
+  if (lane_id() == 0) finish(st, b * a.W + i, a.argmax, a.entropy, a.pmax);
 }
 
-int plan_chunks(int B, int W, int V, int* chunk) {
-  // about 1024 workgroups over the B*W rows (four per CU), each chunk >= 16K
-  // elements: long enough that the per-workgroup merge is a small share,
-  // short enough that loads stay in flight.  With 1024 rows or more, one
-  // chunk per row: no partials and no merge kernel.
-  const int rows = B * W;
-  int nchunk = (1024 + rows - 1) / rows;
-  const int max_by_size = (V + 16383) / 16384;
-  if (nchunk > max_by_size) nchunk = max_by_size;
-  if (nchunk < 1) nchunk = 1;
-  int c = (V + nchunk - 1) / nchunk;
-  c = (c + 3) & ~3;
-  nchunk = (V + c - 1) / c;
-  *chunk = c;
-  return nchunk;
+// Chunks per row at most (0: no chunking, one workgroup per row): with
+// fewer than 768 rows and a vocabulary of more than one 16K chunk.
+int plan_max_nchunk(int B, int W, int V) {
+  if (static_cast<int64_t>(B) * W >= kTargetWgs) return 0;
+  const int n = (V + kMinChunk - 1) / kMinChunk;
+  return n > 1 ? n : 0;
 }
 
 }  // namespace
 
 extern "C" size_t wedlm_score_workspace_size(int32_t B, int32_t W, int32_t V) {
   if (B < 1 || W < 1 || W > WEDLM_MAX_WINDOW || V < 1) return 0;
-  int chunk;
-  const int nchunk = plan_chunks(B, W, V, &chunk);
-  return nchunk > 1 ? static_cast<size_t>(B) * W * nchunk * sizeof(State) : 0;
+  const int mx = plan_max_nchunk(B, W, V);
+  return mx > 0 ? static_cast<size_t>(B) * W * mx * sizeof(State) : 0;
 }
 
 extern "C" int wedlm_score(const float* logits, int64_t row_stride,
@@ -262,7 +359,8 @@ extern "C" int wedlm_score(const float* logits, int64_t row_stride,
   ScoreArgs a{};
   a.logits = logits; a.row_stride = row_stride; a.n_obs = n_obs;
   a.B = B; a.W = W; a.V = V;
-  a.nchunk = plan_chunks(B, W, V, &a.chunk);
+  a.max_nchunk = plan_max_nchunk(B, W, V);
+  a.dyn = a.max_nchunk > 0;
   a.c2 = 1.4426950408889634074 / temperature;
   a.argmax = argmax; a.entropy = entropy; a.pmax = pmax;
   const size_t need = wedlm_score_workspace_size(B, W, V);
@@ -271,14 +369,16 @@ extern "C" int wedlm_score(const float* logits, int64_t row_stride,
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool vec = (row_stride & 3) == 0 &&
                    (reinterpret_cast<uintptr_t>(logits) & 15) == 0;
+  // dyn: at most masked rows x ceil(768 / masked rows) items, i.e. fewer
+  // than 768 + B*W, and at most B*W x max_nchunk
+  const int rows = B * W;
+  const int grid = a.dyn ? std::min(kTargetWgs + rows, rows * a.max_nchunk) : rows;
   if (vec)
-    hipLaunchKernelGGL(score_kernel<true>, dim3(B * W * a.nchunk),
-                       dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL(score_kernel<true>, dim3(grid), dim3(kThreads), 0, st, a);
   else
-    hipLaunchKernelGGL(score_kernel<false>, dim3(B * W * a.nchunk),
-                       dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL(score_kernel<false>, dim3(grid), dim3(kThreads), 0, st, a);
   WEDLM_LAUNCH_CHECK();
-  if (a.nchunk > 1) {
+  if (a.dyn) {
     hipLaunchKernelGGL(score_merge_kernel, dim3(B * W), dim3(kWave), 0, st, a);
     WEDLM_LAUNCH_CHECK();
   }
