@@ -7,9 +7,10 @@ are already resident in HBM.  Every step starts from the workload's own
 window state (a fresh device copy per step, made before the timed region),
 so every timed step does the configured workload's work.
 Small workloads rotate over several input sets so that no timed step finds
-its inputs in the 256 MB last-level cache.  --graph replays each step from a
-HIP graph (the window reset inside it), which removes the host's launch
-gaps from the small workloads' steps.
+its inputs in the 256 MB last-level cache.  --graph replays whole rounds of
+steps over the input sets from HIP graphs (the window resets timed apart and
+subtracted), which removes the host's launch gaps from the small workloads'
+steps.
 
 Prints ONE JSON line: window tokens/s (B*W per step time), the roofline of
 the dominant kernel (window attention: algorithmic bytes per launch over its
@@ -636,7 +637,19 @@ def main():
         for _ in range(5):
             dst.copy_(src)
         torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes": n, "launches": 5}), flush=True)
+        # the measured copy peak: 20 timed copies, read + write bytes
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(20):
+            dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / 20 * 1e3
+        print(json.dumps({"copy_bytes": n, "launches": 25,
+                          "us_per_copy": us,
+                          "copy_gbps_read_plus_write": 2 * n / us / 1e3}),
+              flush=True)
         return
 
     if args.compare_rules:
@@ -698,43 +711,60 @@ def main():
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     if args.graph:
-        # one HIP graph per input set: the set's window state reset from a
-        # stored copy (two small device copies), then the four calls; and
-        # one graph of the attention alone (on its own copy of the prefix
-        # lengths) for the kernel's launch time.  Replays go round the sets.
-        graphs, attn_graphs = [], []
-        for s in sets:
-            init = (s["win_tok"].clone(), s["win_start"].clone())
-            plen = s["win_start"].clone()
-            g, ga = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                s["win_tok"].copy_(init[0])
-                s["win_start"].copy_(init[1])
+        # One HIP graph holds a whole round over the input sets: per set the
+        # window state reset from a stored copy (two small device copies),
+        # then the four calls.  A second graph holds the resets alone; the
+        # step time is the difference of the two, per step, so the resets
+        # are not timed (the eager loop makes its copies before the timed
+        # region).  A third graph holds one attention call per set (on its
+        # own copy of the prefix lengths) for the kernel's time.  Each graph
+        # covers many steps, so the host's graph launches never leave the
+        # GPU waiting.
+        inits = [(s["win_tok"].clone(), s["win_start"].clone(),
+                  s["win_start"].clone()) for s in sets]
+        g_all, g_reset, g_attn = (torch.cuda.CUDAGraph(),
+                                  torch.cuda.CUDAGraph(),
+                                  torch.cuda.CUDAGraph())
+
+        def reset(i):
+            sets[i]["win_tok"].copy_(inits[i][0])
+            sets[i]["win_start"].copy_(inits[i][1])
+
+        with torch.cuda.graph(g_all):
+            for i, s in enumerate(sets):
+                reset(i)
                 step.reorder(s["win_tok"], s["win_start"], s["qkv_in"])
                 step.attn(s["k_cache"], s["v_cache"], s["block_table"],
                           s["win_start"])
                 step.score(s["logits"])
                 step.commit(s["win_tok"], s["win_start"], s["k_cache"],
                             s["v_cache"], s["block_table"])
-            with torch.cuda.graph(ga):
-                step.attn(s["k_cache"], s["v_cache"], s["block_table"], plen)
-            graphs.append(g)
-            attn_graphs.append(ga)
+        with torch.cuda.graph(g_reset):
+            for i in range(n_sets):
+                reset(i)
+        with torch.cuda.graph(g_attn):
+            for i, s in enumerate(sets):
+                step.attn(s["k_cache"], s["v_cache"], s["block_table"],
+                          inits[i][2])
+        rounds = max(1, -(-args.steps // n_sets))
+        warm_rounds = max(1, -(-args.warmup // n_sets))
 
-        def replay_loop(gs):
-            for t in range(args.warmup):
-                gs[t % n_sets].replay()
+        def replay_loop(g):
+            for _ in range(warm_rounds):
+                g.replay()
             torch.cuda.synchronize()
             t_start.record()
-            for t in range(args.steps):
-                gs[t % n_sets].replay()
+            for _ in range(rounds):
+                g.replay()
             t_end.record()
             torch.cuda.synchronize()
             return t_start.elapsed_time(t_end)
 
-        total_ms = replay_loop(graphs)
-        attn_avg_s = replay_loop(attn_graphs) / args.steps / 1e3
-        ms_step = total_ms / args.steps
+        n_timed = rounds * n_sets
+        total_ms = replay_loop(g_all) - replay_loop(g_reset)
+        attn_avg_s = replay_loop(g_attn) / n_timed / 1e3
+        ms_step = total_ms / n_timed
+        args.steps, args.warmup = n_timed, warm_rounds * n_sets
     else:
         # every step starts from the workload's own window: one fresh copy
         # of the window state per step, made before the timed region (the
