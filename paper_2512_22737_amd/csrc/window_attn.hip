@@ -611,17 +611,145 @@ void window_attn_kernel(AttnArgs a) {
           bf16x8_t,
           *reinterpret_cast<const u16x8_t*>(sb + T::k_off(krow, 2 * kk + hf)));
   };
+  // ---- boundary tiles: the partial last prefix tile (keys past k1 or on a
+  // bad page are zeroed and masked), then the window tiles of the last
+  // split (V transposed into V^T on the store).  They are scored before the
+  // full tiles, in the ring's last slot (never among the first LEAD loads),
+  // with their loads issued right after the first LEAD tile loads: the two
+  // round trips overlap, and the boundary work is off the end of the split
+  // (where it used to wait for its own loads after the last full tile).
+  constexpr int kMaxTail = 1 + (WEDLM_MAX_WINDOW + kTileKeys - 1) / kTileKeys;
+  const int n_tail = (partial_last ? 1 : 0) + n_win;
+  constexpr int kTailSlot = NS - 1;
+  static_assert(kTailSlot >= LEAD, "the tail slot is not among the first loads");
+  int tail_lim = 0;
+  u16x8_t tr[kMaxTail][CPT];
+  auto tail_load = [&](int tt, u16x8_t (&r)[CPT]) {
+    const bool is_win = !(partial_last && tt == 0);
+    if (!is_win) {
+      const int base = k0 + n_full * kTileKeys;
+      int pg[2];
+      bool pv2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int id =
+            (base + h * kPage < k1) ? load_uniform(btb, base / kPage + h) : -1;
+        pv2[h] = id >= 0 && id < a.num_pages;
+        if (base + h * kPage < k1 && !pv2[h]) pages_ok = false;
+        pg[h] = pv2[h] ? id : 0;
+      }
+      const int lim =
+          !pv2[0] ? base - 1 : (!pv2[1] ? min(k1, base + kPage) - 1 : k1 - 1);
+      tail_lim = lim;
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int blk = g_blk[u];
+        const int h = blk & 1;
+        const bool isv = blk >= 2;
+        const int64_t pbase =
+            (static_cast<int64_t>(pg[h]) * a.Hkv + kvh) * kPage * D;
+        u16x8_t v = *reinterpret_cast<const u16x8_t*>(
+            (isv ? a.vc : a.kc) + pbase + g_voff[u] / 2);
+        // first key of this chunk: one key per K chunk, eight per V chunk
+        const int c = g_voff[u] / 16;
+        const int kf = isv ? h * kPage + (c % 2) * 8 : h * kPage + c / (D / 8);
+        const u16x8_t z = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (!isv) {
+          v = (base + kf <= lim) ? v : z;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] = (base + kf + e <= lim) ? v[e] : static_cast<uint16_t>(0);
+        }
+        r[u] = v;
+      }
+    } else {
+      const int base = (tt - (partial_last ? 1 : 0)) * kTileKeys;
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int ch = static_cast<int>(threadIdx.x) + u * NT;
+        const bool isv = ch >= kTileKeys * (D / 8);
+        const int c2 = isv ? ch - kTileKeys * (D / 8) : ch;
+        const int key = c2 / (D / 8);
+        const int cc = c2 % (D / 8);
+        u16x8_t v = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (base + key < a.W)
+          v = *reinterpret_cast<const u16x8_t*>(
+              (isv ? a.vw : a.kw) +
+              ((static_cast<int64_t>(b) * a.W + base + key) * a.Hkv + kvh) * D +
+              cc * 8);
+        r[u] = v;
+      }
+    }
+  };
+  auto tail_store = [&](int tt, const u16x8_t (&r)[CPT]) {
+    const bool is_win = !(partial_last && tt == 0);
+    if (!is_win) {
+      stash(r, kTailSlot);
+    } else {
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int ch = static_cast<int>(threadIdx.x) + u * NT;
+        const bool isv = ch >= kTileKeys * (D / 8);
+        const int c2 = isv ? ch - kTileKeys * (D / 8) : ch;
+        const int key = c2 / (D / 8);
+        const int cc = c2 % (D / 8);
+        if (!isv) {
+          *reinterpret_cast<u16x8_t*>(kb(kTailSlot) + T::k_off(key, cc)) = r[u];
+        } else {
+          const int h = key / kPage, kk = key % kPage;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            *reinterpret_cast<uint16_t*>(vb(kTailSlot) +
+                                         T::v_off(h, cc * 8 + e, kk / 8) +
+                                         (kk % 8) * 2) = r[u][e];
+        }
+      }
+    }
+  };
+  auto tail_tiles = [&]() {
+#pragma unroll
+    for (int tt = 0; tt < kMaxTail; ++tt)
+      if (tt < n_tail) tail_load(tt, tr[tt]);
+#pragma unroll
+    for (int tt = 0; tt < kMaxTail; ++tt) {
+      if (tt < n_tail) {
+        const bool is_win = !(partial_last && tt == 0);
+        const int base = is_win ? (tt - (partial_last ? 1 : 0)) * kTileKeys
+                                : k0 + n_full * kTileKeys;
+        __syncthreads();   // every wave is done with the slot's last tile
+        tail_store(tt, tr[tt]);
+        __syncthreads();
+        qk(kTailSlot, sbuf[0]);
+        bf16x8_t pf[QB][2], vf[2][NM];
+        softmax_general(sbuf[0], true, base, tail_lim, is_win, pf);
+        vread(kTailSlot, vf);
+        pv(vf, pf);
+      }
+    }
+    __syncthreads();       // the slot is free for the ring's loads
+  };
   if (n_full > 0) {
 #pragma unroll
     for (int j = 0; j < LEAD; ++j)
       dma_ids(ids_of(min(j, last_full)), j);
+  }
+  if (n_tail > 0) tail_tiles();
+  if (n_full > 0) {
     wait_vmcnt<kInFlight>();
     __syncthreads();
     qk(0, sbuf[0]);
     if constexpr (kHoist) kread(1);
-    // the first tile's max is each column's reference max
+    // the first full tile's max is each column's reference max, or raises
+    // the one the boundary tiles set (the column rescaled)
 #pragma unroll
-    for (int q = 0; q < QB; ++q) m2[q] = col_max(sbuf[0][q]) * c2;
+    for (int q = 0; q < QB; ++q) {
+      const float mx = col_max(sbuf[0][q]) * c2;
+      if (mx > m2[q]) {
+        rescale(q, m2[q] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m2[q] - mx));
+        m2[q] = mx;
+      }
+    }
   }
   // page ids of the next load, read one iteration ahead of their use
   int2 nid = ids_of(min(LEAD, max(last_full, 0)));
@@ -698,88 +826,7 @@ void window_attn_kernel(AttnArgs a) {
   }
 #undef WEDLM_TILE_ITER
 tiles_done:
-  wait_vmcnt<0>();   // surplus fetches retire before the tail reuses stages
-
-  // ---- boundary tiles, one at a time, plain synchronous loads: the
-  // partial last prefix tile (keys past k1 or on a bad page are zeroed and
-  // masked), then the window tiles of the last split (V transposed into
-  // V^T on the store).
-  const int n_tail = (partial_last ? 1 : 0) + n_win;
-  for (int tt = 0; tt < n_tail; ++tt) {
-    const bool is_win = !(partial_last && tt == 0);
-    const int ts = (n_full + tt) % NS;
-    int base, lim = 0;
-    if (!is_win) {
-      base = k0 + n_full * kTileKeys;
-      int pg[2];
-      bool pv2[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int id =
-            (base + h * kPage < k1) ? load_uniform(btb, base / kPage + h) : -1;
-        pv2[h] = id >= 0 && id < a.num_pages;
-        if (base + h * kPage < k1 && !pv2[h]) pages_ok = false;
-        pg[h] = pv2[h] ? id : 0;
-      }
-      lim = !pv2[0] ? base - 1 : (!pv2[1] ? min(k1, base + kPage) - 1 : k1 - 1);
-      u16x8_t r[CPT];
-#pragma unroll
-      for (int u = 0; u < CPT; ++u) {
-        const int blk = g_blk[u];
-        const int h = blk & 1;
-        const bool isv = blk >= 2;
-        const int64_t pbase =
-            (static_cast<int64_t>(pg[h]) * a.Hkv + kvh) * kPage * D;
-        u16x8_t v = *reinterpret_cast<const u16x8_t*>(
-            (isv ? a.vc : a.kc) + pbase + g_voff[u] / 2);
-        // first key of this chunk: one key per K chunk, eight per V chunk
-        const int c = g_voff[u] / 16;
-        const int kf = isv ? h * kPage + (c % 2) * 8 : h * kPage + c / (D / 8);
-        const u16x8_t z = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (!isv) {
-          v = (base + kf <= lim) ? v : z;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            v[e] = (base + kf + e <= lim) ? v[e] : static_cast<uint16_t>(0);
-        }
-        r[u] = v;
-      }
-      __syncthreads();   // every wave is done with the stage being reused
-      stash(r, ts);
-    } else {
-      base = (tt - (partial_last ? 1 : 0)) * kTileKeys;
-      __syncthreads();
-      for (int ch = threadIdx.x; ch < 2 * kTileKeys * (D / 8);
-           ch += NW * kWave) {
-        const bool isv = ch >= kTileKeys * (D / 8);
-        const int c2 = isv ? ch - kTileKeys * (D / 8) : ch;
-        const int key = c2 / (D / 8);
-        const int cc = c2 % (D / 8);
-        u16x8_t v = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (base + key < a.W)
-          v = *reinterpret_cast<const u16x8_t*>(
-              (isv ? a.vw : a.kw) +
-              ((static_cast<int64_t>(b) * a.W + base + key) * a.Hkv + kvh) * D +
-              cc * 8);
-        if (!isv) {
-          *reinterpret_cast<u16x8_t*>(kb(ts) + T::k_off(key, cc)) = v;
-        } else {
-          const int h = key / kPage, kk = key % kPage;
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            *reinterpret_cast<uint16_t*>(vb(ts) + T::v_off(h, cc * 8 + e, kk / 8) +
-                                         (kk % 8) * 2) = v[e];
-        }
-      }
-    }
-    __syncthreads();
-    qk(ts, sbuf[0]);
-    bf16x8_t pf[QB][2], vf[2][NM];
-    softmax_general(sbuf[0], true, base, lim, is_win, pf);
-    vread(ts, vf);
-    pv(vf, pf);
-  }
+  wait_vmcnt<0>();   // surplus fetches retire before the output is written
 
   if (!pages_ok && a.status && threadIdx.x == 0)
     atomicOr(a.status + b, WEDLM_SEQ_BAD_PAGE);
