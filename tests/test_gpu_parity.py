@@ -344,6 +344,70 @@ def test_attention_workspace_reuse():
             assert err.max() <= PL.ATTN_MAX_ABS and rel <= PL.ATTN_REL_NORM
 
 
+def test_attention_workspace_shared_by_shapes():
+    """One workspace, filled with random bytes first, serves calls of two
+    shapes in turn (their split plans place the arrival words and partials
+    at different offsets, so each call's words sit on bytes the other shape
+    wrote), three times over; every output is checked against the oracle.
+    The splits of a query block count their arrivals in those words and the
+    last one merges; bytes left by another call must never count."""
+    import torch
+    from oracle import wedlm_oracle as O
+    from paper_2512_22737_amd import wedlm
+    shapes = [
+        WL.Workload("share_a", 63, B=3, W=48, Hq=8, Hkv=2, D=128, V=300,
+                    prefix=3000, prefix_hi=9000, obs_frac=0.3,
+                    obs_frac_hi=0.6, spike=9.0),
+        WL.Workload("share_b", 64, B=5, W=16, Hq=4, Hkv=2, D=128, V=300,
+                    prefix=800, prefix_hi=2500, obs_frac=0.3,
+                    obs_frac_hi=0.6, spike=9.0),
+    ]
+    runs = []
+    need = 0
+    for wl in shapes:
+        d = WL.step_inputs(wl, seed=1)
+        mp = int(d["win_start"].max())
+        need = max(need, wedlm.wedlm_window_attn_workspace_size(
+            wl.B, wl.W, wl.Hq, wl.Hkv, wl.D, mp))
+        step = wedlm.DecodeStep(wl.B, wl.W, wl.Hq, wl.Hkv, wl.D, wl.V, mp)
+        runs.append((wl, d, PL.to_dev(d), step, mp))
+    assert need > 0
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    ws = torch.randint(0, 256, (need,), dtype=torch.uint8, device="cuda",
+                       generator=g)
+    refs = {}
+    for rnd in range(3):
+        for wl, d, dev, step, mp in runs:
+            PL.log(f"case {wl.name} round {rnd}")
+            step.reorder(dev["win_tok"], dev["win_start"], dev["qkv_in"])
+            out = torch.full_like(step.out, float("nan"))
+            status = torch.zeros_like(step.attn_status)
+            wedlm.wedlm_window_attn(step.q_phys, step.k_phys, step.v_phys,
+                                    dev["k_cache"], dev["v_cache"],
+                                    dev["block_table"], dev["win_start"], mp,
+                                    out, status=status, workspace=ws)
+            torch.cuda.synchronize()
+            assert (status.cpu().numpy() == 0).all()
+            got = out.float().cpu().numpy().astype(np.float64)
+            for b in range(wl.B):
+                key = (wl.name, b)
+                if key not in refs:
+                    c = int(d["win_start"][b])
+                    perm, pos, _, _ = O.reorder(list(d["win_tok"][b]), c)
+                    q, k, v = O.rope_window(d["qkv_in"][b], perm, pos, wl.Hq,
+                                            wl.Hkv, wl.theta)
+                    kp, vp = WL.gather_prefix(d["k_cache"], d["v_cache"],
+                                              d["block_table"], b, c)
+                    refs[key], _ = O.window_attn(q, k, v, O.bf16_to_f64(kp),
+                                                 O.bf16_to_f64(vp))
+                ref = refs[key]
+                err = np.abs(got[b] - ref)
+                rel = np.linalg.norm(got[b] - ref) / np.linalg.norm(ref)
+                assert err.max() <= PL.ATTN_MAX_ABS and rel <= PL.ATTN_REL_NORM, \
+                    (wl.name, rnd, b, float(err.max()), float(rel))
+
+
 def test_attention_status_bits():
     """Device-side checks of wedlm_window_attn: a prefix longer than
     max_prefix_len is reported (WEDLM_SEQ_BAD_LEN) and that sequence is
