@@ -289,6 +289,33 @@ void window_attn_kernel(AttnArgs a) {
   const int kvh = wg % a.Hkv;
   const int b = wg / a.Hkv;
 
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  const int col = lane & 31;        // query column of this lane
+  const int hf = lane >> 5;         // which half of the k slots
+  const int rows = a.W * a.G;
+
+  // ---- queries (B operand of S^T = K . Q^T), issued before the prefix
+  // length is read: their addresses need only the workgroup's indices, so
+  // their round trip overlaps those of the prefix length and page ids
+  int qi[QB], qh[QB];
+  bool rvalid[QB];
+  bf16x8_t qf[QB][NK];
+#pragma unroll
+  for (int q = 0; q < QB; ++q) {
+    const int r = qb * (NW * QB * 32) + (wave * QB + q) * 32 + col;
+    rvalid[q] = r < rows;
+    qi[q] = rvalid[q] ? r / a.G : 0;
+    qh[q] = kvh * a.G + (rvalid[q] ? r % a.G : 0);
+    const uint16_t* qp =
+        a.q + ((static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]) * D;
+    // padded rows (past W*G) read row 0's query; their outputs are dropped
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk)
+      qf[q][kk] = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const u16x8_t*>(qp + kk * 16 + hf * 8));
+  }
+
   int c;
   if (!seq_ok(a, b, c)) {
     if (a.status && threadIdx.x == 0 && split == 0 && qb == 0 && kvh == 0)
@@ -304,11 +331,6 @@ void window_attn_kernel(AttnArgs a) {
   const int n_pre = k1 > k0 ? (k1 - k0 + kTileKeys - 1) / kTileKeys : 0;
   const int n_win = last ? (a.W + kTileKeys - 1) / kTileKeys : 0;
 
-  const int wave = threadIdx.x / kWave;
-  const int lane = lane_id();
-  const int col = lane & 31;        // query column of this lane
-  const int hf = lane >> 5;         // which half of the k slots
-  const int rows = a.W * a.G;
 
   // ---- tile loads.  A tile is four 4 KB blocks (D = 128; 2 KB for
   // D = 64): the K rows of page 0 and page 1, then the V^T rows of page 0
@@ -386,31 +408,6 @@ void window_attn_kernel(AttnArgs a) {
       *reinterpret_cast<u16x8_t*>((g_blk[u] < 2 ? kb(s) : vb(s)) + l_off[u]) =
           r[u];
   };
-
-  // ---- queries (B operand of S^T = K . Q^T)
-  int qi[QB], qh[QB];
-  bool rvalid[QB];
-  bf16x8_t qf[QB][NK];
-#pragma unroll
-  for (int q = 0; q < QB; ++q) {
-    const int r = qb * (NW * QB * 32) + (wave * QB + q) * 32 + col;
-    rvalid[q] = r < rows;
-    qi[q] = rvalid[q] ? r / a.G : 0;
-    qh[q] = kvh * a.G + (rvalid[q] ? r % a.G : 0);
-    const uint16_t* qp =
-        a.q + ((static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]) * D;
-    // padded rows (past W*G) read row 0's query; their outputs are dropped
-#pragma unroll
-    for (int kk = 0; kk < NK; ++kk)
-      qf[q][kk] = __builtin_bit_cast(
-          bf16x8_t, *reinterpret_cast<const u16x8_t*>(qp + kk * 16 + hf * 8));
-  }
-  // take delivery of the queries here, once: later uses then see plain
-  // register values and the tile loop never waits on these loads again
-#pragma unroll
-  for (int q = 0; q < QB; ++q)
-#pragma unroll
-    for (int kk = 0; kk < NK; ++kk) asm volatile("" : "+v"(qf[q][kk]));
 
   floatx16_t o[QB][NM];
 #pragma unroll
@@ -594,6 +591,14 @@ void window_attn_kernel(AttnArgs a) {
     pg_lds[i] = id;
   }
   __syncthreads();
+  // take delivery of the queries here, once (they were issued at the top and
+  // have long arrived): later uses then see plain register values and the
+  // tile loop never waits on these loads again
+#pragma unroll
+  for (int q = 0; q < QB; ++q)
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) asm volatile("" : "+v"(qf[q][kk]));
+
   // Tiles published at a barrier: with the K fragments one step ahead and
   // a barrier every two iterations, every tile up to t+4; without them and
   // a barrier every iteration, every tile up to t+2.
@@ -899,23 +904,26 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
   const int bk = static_cast<int>(gr / rows);
   const int kvh = bk % a.Hkv;
   const int b = bk / a.Hkv;
-  int c;
-  if (!seq_ok(a, b, c)) return;
-  const int nsplit_b = seq_split(c, a.nsplit).n;
   const int d = (threadIdx.x % TPR) * 8;
   const int64_t rows_base =
       (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
   const float2* ml = a.ws_ml + rows_base * a.nsplit;
   const uint16_t* op = a.ws_o + rows_base * a.nsplit * D + d;
+  // the first min(nsplit, 8) slots are loaded before the prefix length is
+  // known (slots past this sequence's splits are in the workspace and their
+  // values are never used), so both round trips overlap
   float2 mls[kMaxFast];
   u16x8_t vs[kMaxFast];
 #pragma unroll
   for (int s = 0; s < kMaxFast; ++s) {
-    if (s < nsplit_b) {
+    if (s < a.nsplit) {
       mls[s] = ml[s];
       vs[s] = *reinterpret_cast<const u16x8_t*>(op + static_cast<int64_t>(s) * D);
     }
   }
+  int c;
+  if (!seq_ok(a, b, c)) return;
+  const int nsplit_b = seq_split(c, a.nsplit).n;
   float M = kNegInf;
 #pragma unroll
   for (int s = 0; s < kMaxFast; ++s)
