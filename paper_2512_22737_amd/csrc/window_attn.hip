@@ -788,7 +788,7 @@ void window_attn_kernel(AttnArgs a) {
     _Pragma("unroll")                                                     \
     for (int i = 0; i < NK * QB; ++i) {                                   \
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   /* one MFMA  */\
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   /* four VALU */\
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   /* two VALU  */\
     }                                                                     \
     {                                                                     \
       bool big = false;                                                   \
