@@ -42,6 +42,16 @@ __device__ __forceinline__ uint64_t ballot(bool p) {
 // Lane index within the wave.
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
+// Element (t, k) of an activation matrix with K columns (a multiple of 64)
+// in the packed MFMA tile layout of the projections: tile (t/32, k/64) at
+// 2048 * (t/32 * K/64 + k/64), then MFMA j = k%32 / 8 (512 elements each),
+// lane t%32 + 32 * (k%64 / 32), element k%8.  Eight consecutive k from a
+// multiple of 8 are 16 contiguous bytes.
+__device__ __forceinline__ int64_t packed_off(int64_t t, int k, int K) {
+  return ((t / 32 * (K / 64) + k / 64) * 4 + (k & 31) / 8) * 512 +
+         ((t & 31) + 32 * ((k & 63) / 32)) * 8 + (k & 7);
+}
+
 }  // namespace wedlm
 
 // Host-side launch check.

@@ -29,8 +29,10 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
+#include "internal.h"
 #include "wedlm_model.h"
 
 using namespace wedlm;
@@ -38,15 +40,6 @@ using namespace wedlm;
 namespace {
 
 constexpr int kKStep = 64;                        // k per MFMA step (4 x 16)
-
-// Element (t, k) of an activation matrix with K columns in the packed tile
-// layout (the weights' layout applied to rows of tokens): tile (t/32, k/64)
-// at 2048 * (t/32 * K/64 + k/64), lane t%32 + 32 * (k%64 / 32), MFMA j =
-// k%32 / 8, element k%8.
-__device__ __forceinline__ int64_t tile_off(int64_t t, int k, int K) {
-  return ((t / 32 * (K / kKStep) + k / kKStep) * 4 + (k & 31) / 8) * 512 +
-         ((t & 31) + 32 * ((k & 63) / 32)) * 8 + (k & 7);
-}
 
 // ---------------------------------------------------------------------------
 // embedding: x[t] = E[token], [M] -> the mask row; fp32 residual stream
@@ -79,49 +72,125 @@ __global__ __launch_bounds__(256) void embed_kernel(
 // With ADD, the n_ks partial products of a split residual-add projection
 // ([n_ks, M, Hd] fp32) are first added into x in split order and the sum is
 // written back (the residual stream), then normalised.
+// A thread owns the float4 chunks c = tid + 256 i, i < CPT, of its row and
+// keeps them in registers: the loads of x, of the gain and of up to
+// kNormPre partials are all issued before the first add, so a row costs one
+// memory round trip before the reduction (CPT = 0: rows longer than 8192,
+// a loop over the chunks).
 // ---------------------------------------------------------------------------
 constexpr int kNormThreads = 256;
+constexpr int kNormPre = 4;
 
-template <bool ADD, bool XP>
+template <bool ADD, bool XP, int CPT>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
     float* __restrict__ x, const float* __restrict__ part, int n_ks, int M,
     const uint16_t* __restrict__ g, int Hd, float eps,
     uint16_t* __restrict__ y) {
   const int t = blockIdx.x;
+  const int nc = Hd / 4;
   float* row = x + static_cast<int64_t>(t) * Hd;
-  float ss = 0.f;
-  for (int c = threadIdx.x; c < Hd / 4; c += kNormThreads) {
-    floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
-    if constexpr (ADD) {
-      for (int k = 0; k < n_ks; ++k) {
-        const floatx4_t p = *reinterpret_cast<const floatx4_t*>(
-            part + (static_cast<int64_t>(k) * M + t) * Hd + c * 4);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] += p[e];
-      }
-      *reinterpret_cast<floatx4_t*>(row + c * 4) = v;
-    }
-    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-  __shared__ float wsum[kNormThreads / kWave];
-  if (lane_id() == 0) wsum[threadIdx.x / kWave] = ss;
-  __syncthreads();
-  float tot = 0.f;
-#pragma unroll
-  for (int i = 0; i < kNormThreads / kWave; ++i) tot += wsum[i];
-  const float r = 1.0f / sqrtf(tot / static_cast<float>(Hd) + eps);
   uint16_t* out = y + static_cast<int64_t>(t) * Hd;   // row-major
-  // every thread re-reads only the chunks it wrote itself
-  for (int c = threadIdx.x; c < Hd / 4; c += kNormThreads) {
-    const floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
-    const u16x4_t gg = *reinterpret_cast<const u16x4_t*>(g + c * 4);
+  auto store_out = [&](int c, const floatx4_t& v, const u16x4_t& gg, float r) {
     u16x4_t o;
 #pragma unroll
     for (int e = 0; e < 4; ++e) o[e] = f32_to_bf16(v[e] * r * bf16_to_f32(gg[e]));
     // packed (XP): the 4 values share one 16-byte chunk of a tile
-    *reinterpret_cast<u16x4_t*>(XP ? y + tile_off(t, c * 4, Hd) : out + c * 4) = o;
+    *reinterpret_cast<u16x4_t*>(XP ? y + packed_off(t, c * 4, Hd) : out + c * 4) = o;
+  };
+  __shared__ float wsum[kNormThreads / kWave];
+  auto row_total = [&](float ss) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+    if (lane_id() == 0) wsum[threadIdx.x / kWave] = ss;
+    __syncthreads();
+    float tot = 0.f;
+#pragma unroll
+    for (int i = 0; i < kNormThreads / kWave; ++i) tot += wsum[i];
+    return 1.0f / sqrtf(tot / static_cast<float>(Hd) + eps);
+  };
+
+  if constexpr (CPT > 0) {
+    floatx4_t v[CPT];
+    u16x4_t gg[CPT];
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = threadIdx.x + i * kNormThreads;
+      if (c < nc) {
+        v[i] = *reinterpret_cast<const floatx4_t*>(row + c * 4);
+        gg[i] = *reinterpret_cast<const u16x4_t*>(g + c * 4);
+      }
+    }
+    if constexpr (ADD) {
+      floatx4_t p[kNormPre][CPT];
+#pragma unroll
+      for (int k = 0; k < kNormPre; ++k)
+        if (k < n_ks)
+#pragma unroll
+          for (int i = 0; i < CPT; ++i) {
+            const int c = threadIdx.x + i * kNormThreads;
+            if (c < nc)
+              p[k][i] = *reinterpret_cast<const floatx4_t*>(
+                  part + (static_cast<int64_t>(k) * M + t) * Hd + c * 4);
+          }
+      // split order: x + p_0 + p_1 + ...
+#pragma unroll
+      for (int k = 0; k < kNormPre; ++k)
+        if (k < n_ks)
+#pragma unroll
+          for (int i = 0; i < CPT; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[i][e] += p[k][i][e];
+      for (int k = kNormPre; k < n_ks; ++k)
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) {
+          const int c = threadIdx.x + i * kNormThreads;
+          if (c < nc) {
+            const floatx4_t q = *reinterpret_cast<const floatx4_t*>(
+                part + (static_cast<int64_t>(k) * M + t) * Hd + c * 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[i][e] += q[e];
+          }
+        }
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int c = threadIdx.x + i * kNormThreads;
+        if (c < nc) *reinterpret_cast<floatx4_t*>(row + c * 4) = v[i];
+      }
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = threadIdx.x + i * kNormThreads;
+      if (c < nc)
+        ss += v[i][0] * v[i][0] + v[i][1] * v[i][1] + v[i][2] * v[i][2] +
+              v[i][3] * v[i][3];
+    }
+    const float r = row_total(ss);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = threadIdx.x + i * kNormThreads;
+      if (c < nc) store_out(c, v[i], gg[i], r);
+    }
+  } else {
+    float ss = 0.f;
+    for (int c = threadIdx.x; c < nc; c += kNormThreads) {
+      floatx4_t v = *reinterpret_cast<const floatx4_t*>(row + c * 4);
+      if constexpr (ADD) {
+        for (int k = 0; k < n_ks; ++k) {
+          const floatx4_t p = *reinterpret_cast<const floatx4_t*>(
+              part + (static_cast<int64_t>(k) * M + t) * Hd + c * 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += p[e];
+        }
+        *reinterpret_cast<floatx4_t*>(row + c * 4) = v;
+      }
+      ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+    }
+    const float r = row_total(ss);
+    // every thread re-reads only the chunks it wrote itself
+    for (int c = threadIdx.x; c < nc; c += kNormThreads)
+      store_out(c, *reinterpret_cast<const floatx4_t*>(row + c * 4),
+                *reinterpret_cast<const u16x4_t*>(g + c * 4), r);
   }
 }
 
@@ -182,6 +251,25 @@ __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
   const int H = Hq + 2 * Hkv;
   const int64_t row = static_cast<int64_t>(t) * H * D;   // element offset
   const int64_t pstride = static_cast<int64_t>(M) * H * D;
+  const int nv = Hkv * D / 8;                     // 16-byte pieces of v
+  // the first two rounds of q/k items and the first round of v are loaded
+  // before the rotation table is computed, so its fp64 trigonometry runs
+  // under their round trip
+  auto load_item = [&](int it, u16x8_t& lo8, u16x8_t& hi8) {
+    if (it < n_items) {
+      const int head = it / per_head;
+      const int j0 = (it - head * per_head) * 8;
+      lo8 = qkv_load8<PART>(qkv, part, pstride, n_ks, row + head * D + j0);
+      hi8 = qkv_load8<PART>(qkv, part, pstride, n_ks, row + head * D + j0 + half);
+    }
+  };
+  u16x8_t lo0 = {}, hi0 = {}, lo1 = {}, hi1 = {}, v0 = {};
+  load_item(threadIdx.x, lo0, hi0);
+  load_item(threadIdx.x + kQkThreads, lo1, hi1);
+  if (threadIdx.x < nv)
+    v0 = qkv_load8<PART>(qkv, part, pstride, n_ks,
+                         row + (Hq + Hkv) * D + threadIdx.x * 8);
+
   __shared__ double s_cos[kMaxHalf], s_sin[kMaxHalf];
   if (threadIdx.x < half) {
     const int j = threadIdx.x;
@@ -195,16 +283,10 @@ __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
   __syncthreads();
   // n_items is a multiple of per_head and every round starts at a multiple
   // of kQkThreads, so a head's items never straddle a round or a wave
-  for (int base = 0; base < n_items; base += kQkThreads) {
-    const int it = base + threadIdx.x;
+  auto rotate = [&](int it, const u16x8_t& lo8, const u16x8_t& hi8) {
     const bool live = it < n_items;
     const int head = live ? it / per_head : 0;
     const int j0 = live ? (it - head * per_head) * 8 : 0;
-    u16x8_t lo8 = {}, hi8 = {};
-    if (live) {
-      lo8 = qkv_load8<PART>(qkv, part, pstride, n_ks, row + head * D + j0);
-      hi8 = qkv_load8<PART>(qkv, part, pstride, n_ks, row + head * D + j0 + half);
-    }
     float a[8], b[8], ss = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -213,7 +295,7 @@ __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
       ss += a[e] * a[e] + b[e] * b[e];
     }
     for (int off = 1; off < per_head; off <<= 1) ss += __shfl_xor(ss, off);
-    if (!live) continue;
+    if (!live) return;
     const float r = 1.0f / sqrtf(ss / static_cast<float>(D) + eps);
     const uint16_t* g = head < Hq ? gq : gk;
     u16x8_t olo, ohi;
@@ -230,10 +312,18 @@ __global__ __launch_bounds__(kQkThreads) void qk_norm_rope_kernel(
                         : k_out + (static_cast<int64_t>(t) * Hkv + head - Hq) * D;
     *reinterpret_cast<u16x8_t*>(dst + j0) = olo;
     *reinterpret_cast<u16x8_t*>(dst + j0 + half) = ohi;
+  };
+  rotate(threadIdx.x, lo0, hi0);
+  if (n_items > kQkThreads) rotate(threadIdx.x + kQkThreads, lo1, hi1);
+  for (int base = 2 * kQkThreads; base < n_items; base += kQkThreads) {
+    u16x8_t lo8 = {}, hi8 = {};
+    load_item(base + threadIdx.x, lo8, hi8);
+    rotate(base + threadIdx.x, lo8, hi8);
   }
   u16x8_t* dv =
       reinterpret_cast<u16x8_t*>(v_out + static_cast<int64_t>(t) * Hkv * D);
-  for (int e = threadIdx.x; e < Hkv * D / 8; e += kQkThreads)
+  if (threadIdx.x < nv) dv[threadIdx.x] = v0;
+  for (int e = threadIdx.x + kQkThreads; e < nv; e += kQkThreads)
     dv[e] = qkv_load8<PART>(qkv, part, pstride, n_ks, row + (Hq + Hkv) * D + e * 8);
 }
 
@@ -272,7 +362,7 @@ __device__ __forceinline__ void gemm_store(const GemmArgs& a, int tok, int n,
   } else {
     const uint16_t r = f32_to_bf16(g / (1.0f + expf(-g)) * u);
     if constexpr (XP)
-      static_cast<uint16_t*>(a.out)[tile_off(tok, n, a.N)] = r;
+      static_cast<uint16_t*>(a.out)[packed_off(tok, n, a.N)] = r;
     else
       static_cast<uint16_t*>(a.out)[o] = r;
   }
@@ -603,7 +693,7 @@ __global__ __launch_bounds__(kGThreads) void gemm2d_kernel(Gemm2dArgs a) {
           o[r] = f32_to_bf16(gg / (1.0f + expf(-gg)) * uu);
         }
         *reinterpret_cast<u16x4_t*>(static_cast<uint16_t*>(a.out) +
-                                    tile_off(tok, f, a.N)) = o;
+                                    packed_off(tok, f, a.N)) = o;
       } else {
 #pragma unroll
         for (int fi = 0; fi < 2; ++fi) {
@@ -655,26 +745,6 @@ __global__ __launch_bounds__(256) void sum_partials_bf16_kernel(
 #pragma unroll
   for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(v[r]);
   *reinterpret_cast<u16x4_t*>(out + t * ldo + n) = h;
-}
-
-// rows past M in the last tile are zero: a row-major activation matrix
-// [M, K] -> packed tiles (ceil(M/32) of them)
-__global__ __launch_bounds__(256) void pack_rows_kernel(
-    const uint16_t* __restrict__ x, int M, int K, int64_t n_chunks,
-    uint16_t* __restrict__ packed) {
-  const int64_t c = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (c >= n_chunks) return;
-  const int S = K / kKStep;
-  const int64_t tile = c >> 8;
-  const int idx = static_cast<int>(c & 255);
-  const int u = idx >> 6, l = idx & 63;
-  const int64_t rb = tile / S;
-  const int s = static_cast<int>(tile - rb * S);
-  const int64_t row = rb * 32 + (l & 31);
-  const int k = s * kKStep + (l >> 5) * 32 + u * 8;
-  u16x8_t v = {0, 0, 0, 0, 0, 0, 0, 0};
-  if (row < M) v = *reinterpret_cast<const u16x8_t*>(x + row * K + k);
-  *reinterpret_cast<u16x8_t*>(packed + c * 8) = v;
 }
 
 // row-major [rows, K] -> packed MFMA tiles; one thread moves 16 bytes and
@@ -874,8 +944,21 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
 int norm(float* x, const float* part, int n_ks, int M, int Hd,
          const uint16_t* g, float eps, uint16_t* y, bool xp, hipStream_t st) {
   const bool add = part && n_ks > 1;
-  auto k = add ? (xp ? rmsnorm_kernel<true, true> : rmsnorm_kernel<true, false>)
-               : (xp ? rmsnorm_kernel<false, true> : rmsnorm_kernel<false, false>);
+  const int nc = Hd / 4;
+  const int cpt = nc <= kNormThreads ? 1 : nc <= 2 * kNormThreads ? 2
+                  : nc <= 4 * kNormThreads ? 4 : nc <= 8 * kNormThreads ? 8 : 0;
+  using K = void (*)(float*, const float*, int, int, const uint16_t*, int,
+                     float, uint16_t*);
+  auto pick = [&](auto tag) -> K {
+    constexpr int C = decltype(tag)::value;
+    return add ? (xp ? rmsnorm_kernel<true, true, C> : rmsnorm_kernel<true, false, C>)
+               : (xp ? rmsnorm_kernel<false, true, C> : rmsnorm_kernel<false, false, C>);
+  };
+  const K k = cpt == 1   ? pick(std::integral_constant<int, 1>{})
+              : cpt == 2 ? pick(std::integral_constant<int, 2>{})
+              : cpt == 4 ? pick(std::integral_constant<int, 4>{})
+              : cpt == 8 ? pick(std::integral_constant<int, 8>{})
+                         : pick(std::integral_constant<int, 0>{});
   hipLaunchKernelGGL(k, dim3(M), dim3(kNormThreads), 0, st, x,
                      add ? part : nullptr, add ? n_ks : 0, M, g, Hd, eps, y);
   WEDLM_LAUNCH_CHECK();
@@ -912,7 +995,7 @@ bool config_ok(const wedlm_model_config* c) {
 
 // workspace carve-up of the forward, 256-byte aligned pieces
 struct Carve {
-  size_t part, x, xn, qkv, q, attn, attn_p, act, attn_ws, lm_ws, total;
+  size_t part, x, xn, qkv, q, attn, act, attn_ws, lm_ws, total;
   size_t part_bytes;
 };
 
@@ -926,10 +1009,9 @@ Carve carve(const wedlm_model_config* c, int B, int W, int max_prefix_len) {
   // split partials of the two residual-add products (each is summed by the
   // next RMSNorm before the other is written)
   const int Mi = static_cast<int>(M);
-  const bool big = Mi >= k2dMinRows;   // o's input packed (2-D kernel)
   // and of the q|k|v product (summed by the q/k norm that reads it)
   k.part_bytes = std::max(
-      std::max(gemm_plan(Mi, c->hidden, c->n_heads * c->head_dim, kAddF32, big)
+      std::max(gemm_plan(Mi, c->hidden, c->n_heads * c->head_dim, kAddF32, true)
                    .part_bytes,
                gemm_plan(Mi, c->hidden, c->inter, kAddF32, true).part_bytes),
       gemm_plan(Mi, (c->n_heads + 2 * c->n_kv_heads) * c->head_dim, c->hidden,
@@ -940,9 +1022,7 @@ Carve carve(const wedlm_model_config* c, int B, int W, int max_prefix_len) {
   k.xn = off;   off += up256(Mp * Hd * 2);
   k.qkv = off;  off += up256(M * (Hq + 2 * Hkv) * D * 2);
   k.q = off;    off += up256(M * Hq * D * 2);
-  k.attn = off; off += up256(M * Hq * D * 2);
-  k.attn_p = off;   // packed copy of attn for the 2-D kernel
-  off += M >= static_cast<size_t>(k2dMinRows) ? up256(Mp * Hq * D * 2) : 0;
+  k.attn = off; off += up256(Mp * Hq * D * 2);   // packed tiles
   k.act = off;  off += up256(Mp * c->inter * 2);
   k.attn_ws = off;
   off += up256(wedlm_window_attn_workspace_size(B, W, c->n_heads,
@@ -1071,8 +1151,6 @@ extern "C" int wedlm_model_forward(
   uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + cv.qkv);
   uint16_t* q = reinterpret_cast<uint16_t*>(ws + cv.q);
   uint16_t* attn = reinterpret_cast<uint16_t*>(ws + cv.attn);
-  uint16_t* attn_p = reinterpret_cast<uint16_t*>(ws + cv.attn_p);
-  const bool big = B * W >= k2dMinRows;
   uint16_t* act = reinterpret_cast<uint16_t*>(ws + cv.act);
   float* part = reinterpret_cast<float*>(ws + cv.part);
   const size_t part_bytes = cv.part_bytes;
@@ -1117,22 +1195,14 @@ extern "C" int wedlm_model_forward(
                            wt->k_norm + static_cast<int64_t>(l) * D, pos_ids,
                            Hq, Hkv, D, cfg->rope_theta, cfg->rms_eps, q, kl,
                            vl, st));
-    WEDLM_TRY(wedlm_window_attn(
+    // the attention writes its output in the packed tile layout that the
+    // output projection reads
+    WEDLM_TRY(window_attn_packed(
         q, kl, vl, k_cache + l * cache_stride, v_cache + l * cache_stride,
         num_pages, block_table, max_pages, win_start, B, W, Hq, Hkv, D,
-        max_prefix_len, scale, attn, nullptr, status, attn_ws, attn_ws_bytes,
-        stream));
-    const uint16_t* o_in = attn;
-    if (big) {
-      // many rows: o's input goes packed into the 2-D kernel
-      const int64_t chunks = static_cast<int64_t>((M + 31) / 32) * 32 * Hq * D / 8;
-      hipLaunchKernelGGL(pack_rows_kernel, dim3((chunks + 255) / 256),
-                         dim3(256), 0, st, attn, M, Hq * D, chunks, attn_p);
-      WEDLM_LAUNCH_CHECK();
-      o_in = attn_p;
-    }
-    WEDLM_TRY(gemm(o_in, wt->w_o + static_cast<int64_t>(l) * Hd * Hq * D, M,
-                   Hd, Hq * D, x, Hd, kAddF32, part, part_bytes, true, big,
+        max_prefix_len, scale, attn, status, attn_ws, attn_ws_bytes, stream));
+    WEDLM_TRY(gemm(attn, wt->w_o + static_cast<int64_t>(l) * Hd * Hq * D, M,
+                   Hd, Hq * D, x, Hd, kAddF32, part, part_bytes, true, true,
                    st, &pend));
     WEDLM_TRY(norm(x, part, pend, M, Hd,
                    wt->mlp_norm + static_cast<int64_t>(l) * Hd, cfg->rms_eps,

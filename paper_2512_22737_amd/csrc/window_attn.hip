@@ -35,6 +35,7 @@
 // per (sequence, kv head, query block); W*G query rows per kv head give an
 // arithmetic intensity of W*G flop/byte (256 at W=64, G=4).
 #include "common.h"
+#include "internal.h"
 
 #include <mutex>
 
@@ -60,7 +61,7 @@ struct AttnArgs {
   const uint16_t* vc;     // [P, Hkv, D, 16]
   const int32_t* bt;      // [B, max_pages]
   const int32_t* plen;    // [B]
-  uint16_t* out;          // [B, W, Hq, D]
+  uint16_t* out;          // [B, W, Hq, D], or packed tiles (packed != 0)
   float* lse;             // [B, W, Hq] or null
   int32_t* status;        // [B] or null
   uint16_t* ws_o;         // [B, Hkv, rows_pad, nsplit, D] bf16, normalised
@@ -68,6 +69,7 @@ struct AttnArgs {
   int64_t num_pages;
   int B, W, Hq, Hkv, G, max_pages, max_prefix, nsplit, qblocks,
       rows_pad;
+  int packed;             // out as the B*W x Hq*D matrix in packed MFMA tiles
   float scale_log2;       // softmax_scale * log2(e)
 };
 
@@ -847,8 +849,8 @@ tiles_done:
         (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
     if (a.nsplit == 1) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      uint16_t* op =
-          a.out + ((static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]) * D;
+      const int64_t t = static_cast<int64_t>(b) * a.W + qi[q];
+      uint16_t* op = a.out + (t * a.Hq + qh[q]) * D;
 #pragma unroll
       for (int m = 0; m < NM; ++m)
 #pragma unroll
@@ -858,7 +860,9 @@ tiles_done:
                              f32_to_bf16(o[q][m][g4 * 4 + 1] * inv),
                              f32_to_bf16(o[q][m][g4 * 4 + 2] * inv),
                              f32_to_bf16(o[q][m][g4 * 4 + 3] * inv)};
-          *reinterpret_cast<u16x4_t*>(op + d) = v;
+          *reinterpret_cast<u16x4_t*>(
+              a.packed ? a.out + packed_off(t, qh[q] * D + d, a.Hq * D)
+                       : op + d) = v;
         }
       if (a.lse && hf == 0)
         a.lse[(static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]] =
@@ -950,12 +954,15 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
   }
   const int qi = r / a.G;
   const int qh = kvh * a.G + r % a.G;
-  const int64_t orow = (static_cast<int64_t>(b) * a.W + qi) * a.Hq + qh;
+  const int64_t t = static_cast<int64_t>(b) * a.W + qi;
+  const int64_t orow = t * a.Hq + qh;
   const float inv = L > 0.f ? 1.f / L : 0.f;
   u16x8_t o8;
 #pragma unroll
   for (int k = 0; k < 8; ++k) o8[k] = f32_to_bf16(acc[k] * inv);
-  *reinterpret_cast<u16x8_t*>(a.out + orow * D + d) = o8;
+  *reinterpret_cast<u16x8_t*>(
+      a.packed ? a.out + packed_off(t, qh * D + d, a.Hq * D)
+               : a.out + orow * D + d) = o8;
   if (a.lse && d == 0) a.lse[orow] = (M + __log2f(L)) * kLn2;
 }
 
@@ -1030,8 +1037,10 @@ int window_attn_impl(
     const int32_t* block_table, int32_t max_pages, const int32_t* prefix_len,
     int32_t B, int32_t W, int32_t Hq, int32_t Hkv, int32_t D,
     int32_t max_prefix_len, float softmax_scale, uint16_t* out, float* lse,
-    int32_t* status, const Plan& p, void* workspace, hipStream_t st) {
+    int32_t* status, const Plan& p, void* workspace, hipStream_t st,
+    bool packed = false) {
   AttnArgs a{};
+  a.packed = packed ? 1 : 0;
   a.q = q_phys; a.kw = k_phys; a.vw = v_phys; a.kc = k_cache; a.vc = v_cache;
   a.bt = block_table; a.plen = prefix_len; a.out = out; a.lse = lse;
   a.status = status;
@@ -1133,4 +1142,30 @@ extern "C" int wedlm_window_attn(
                           Hq, Hkv, D, max_prefix_len, softmax_scale, out, lse,
                           status, p, workspace,
                           static_cast<hipStream_t>(stream));
+}
+
+// wedlm_window_attn with the output in the packed MFMA tile layout of the
+// projections (the B*W x Hq*D matrix, ceil(B*W/32) row tiles; rows past B*W
+// are not written), for the decoder, whose output projection reads it so.
+int wedlm::window_attn_packed(
+    const uint16_t* q_phys, const uint16_t* k_phys, const uint16_t* v_phys,
+    const uint16_t* k_cache, const uint16_t* v_cache, int64_t num_pages,
+    const int32_t* block_table, int32_t max_pages, const int32_t* prefix_len,
+    int32_t B, int32_t W, int32_t Hq, int32_t Hkv, int32_t D,
+    int32_t max_prefix_len, float softmax_scale, uint16_t* out_packed,
+    int32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
+  const int e = check_args(q_phys, k_phys, v_phys, k_cache, v_cache,
+                           num_pages, block_table, max_pages, prefix_len, B,
+                           W, Hq, Hkv, D, max_prefix_len, softmax_scale,
+                           out_packed);
+  if (e != WEDLM_OK) return e;
+  if ((static_cast<int64_t>(Hq) * D) % 64 != 0) return WEDLM_E_SHAPE;
+  const Plan p = make_plan(B, W, Hq, Hkv, D, max_prefix_len);
+  if (workspace_bytes < p.ws_bytes || (p.ws_bytes && !workspace))
+    return WEDLM_E_WORKSPACE;
+  return window_attn_impl(q_phys, k_phys, v_phys, k_cache, v_cache,
+                          num_pages, block_table, max_pages, prefix_len, B, W,
+                          Hq, Hkv, D, max_prefix_len, softmax_scale,
+                          out_packed, nullptr, status, p, workspace,
+                          static_cast<hipStream_t>(stream), true);
 }

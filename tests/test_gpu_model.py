@@ -76,7 +76,10 @@ def test_embed_exact():
     assert np.array_equal(x.cpu().double().numpy(), ref)
 
 
-@pytest.mark.parametrize("M,Hd", [(1, 256), (7, 4096), (33, 1000), (3, 8192)])
+# Hd up to 8192 in registers (1, 2, 4 or 8 float4 chunks per thread, the
+# last one partly masked at 1000), longer rows through the chunk loop
+@pytest.mark.parametrize("M,Hd", [(1, 256), (7, 4096), (33, 1000), (3, 8192),
+                                  (2, 2048), (2, 12288)])
 def test_rmsnorm(M, Hd):
     w = W_()
     rng = np.random.default_rng(M)
@@ -91,7 +94,10 @@ def test_rmsnorm(M, Hd):
     assert (err <= 2.0 ** -8 * np.abs(ref) + 1e-6).all(), err.max()
 
 
-@pytest.mark.parametrize("M,Hq,Hkv,D", [(5, 4, 2, 64), (33, 32, 8, 128)])
+# one round of q/k items, two rounds, and three with more than 256 pieces of
+# v (the first round of each is loaded before the rotation table)
+@pytest.mark.parametrize("M,Hq,Hkv,D", [(5, 4, 2, 64), (33, 32, 8, 128),
+                                        (2, 64, 32, 128)])
 def test_qk_norm_rope(M, Hq, Hkv, D):
     w = W_()
     rng = np.random.default_rng(D + M)
