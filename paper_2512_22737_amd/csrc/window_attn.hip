@@ -49,6 +49,8 @@ constexpr int kTileKeys = 32;       // keys per LDS tile (two 16-token pages)
 // wait on the LDS reads a full drain).  A split is at most this many pages.
 constexpr int kMaxSplitPages = 2048;
 constexpr float kLn2 = 0.69314718055994530942f;
+// A prefix split holds at least this many 32-key tiles.
+constexpr int kMinSplitTiles = 8;
 // A column's running sum may reach this before its reference max is raised
 // (every term 2^(s - m) is then at most 2^64, far inside fp32).
 constexpr float kSumLimit = 18446744073709551616.0f;  // 2^64
@@ -102,7 +104,7 @@ Plan make_plan(int B, int W, int Hq, int Hkv, int D, int max_prefix) {
   p.rows_pad = p.qblocks * p.rows_per_wg;
   const int tiles = (max_prefix + kTileKeys - 1) / kTileKeys;
   const int base = B * Hkv * p.qblocks;
-  const int max_split = tiles / 8 > 1 ? tiles / 8 : 1;  // >= 8 tiles each
+  const int max_split = tiles / kMinSplitTiles > 1 ? tiles / kMinSplitTiles : 1;
   // Four-wave workgroups run two per CU when the grid reaches 512 (every
   // SIMD then holds two waves): without splitting, or by splitting when
   // the prefix bound allows 32 tiles per split (shorter prefixes measured
@@ -145,7 +147,7 @@ struct SeqSplit {
 
 __device__ __forceinline__ SeqSplit seq_split(int c, int nsplit) {
   const int tiles = (c + kTileKeys - 1) / kTileKeys;
-  int n = tiles / 8;
+  int n = tiles / kMinSplitTiles;
   n = n < 1 ? 1 : (n > nsplit ? nsplit : n);
   const int per = tiles > 0 ? (tiles + n - 1) / n : 1;
   SeqSplit r;
@@ -888,70 +890,88 @@ tiles_done:
   }
 }
 
-// Merge of the split partials: D/8 threads per (b, kv head, row), each
-// owning eight consecutive d (one 16-byte load per split), 256 threads per
-// workgroup.  O = sum_s 2^(m_s - M) l_s O_s / sum_s 2^(m_s - M) l_s over the
-// splits s of the row (O_s normalised by l_s).  The (m, l) pairs and up to
-// eight partial vectors are loaded before any is used, so one memory round
-// trip covers the row.
+// Merge of the split partials: D/8 threads per (b, kv head, row) and slot
+// group, each owning eight consecutive d (one 16-byte load per split); the
+// SG slot groups of a row take the splits s = sg, sg + SG, ... and sit on
+// neighbouring lanes of one wave.  O = sum_s 2^(m_s - M) l_s O_s /
+// sum_s 2^(m_s - M) l_s over the splits s of the row (O_s normalised by
+// l_s).  Every thread loads its (m, l) pairs and up to eight partial
+// vectors before any is used, so one memory round trip covers up to 8 SG
+// splits; the max and the sums are then combined across the slot groups
+// with lane exchanges, in a fixed order.
 constexpr int kCombineThreads = 256;
 
-template <int D>
+template <int D, int SG>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs a) {
-  constexpr int TPR = D / 8;                       // threads per row
-  constexpr int RPW = kCombineThreads / TPR;       // rows per workgroup
-  constexpr int kMaxFast = 8;
+  constexpr int TPR = D / 8;                       // d groups of a row
+  constexpr int TPW = TPR * SG;                    // threads per row
+  static_assert(TPW <= kWave && kWave % TPW == 0, "a row within one wave");
+  constexpr int RPW = kCombineThreads / TPW;       // rows per workgroup
+  constexpr int kFast = 8;                         // slots per thread at once
   const int rows = a.W * a.G;
-  const int64_t gr = static_cast<int64_t>(blockIdx.x) * RPW + threadIdx.x / TPR;
+  const int64_t gr = static_cast<int64_t>(blockIdx.x) * RPW + threadIdx.x / TPW;
+  // whole rows (aligned groups of TPW lanes) leave together, so the lane
+  // exchanges below only ever read lanes of the same row
   if (gr >= static_cast<int64_t>(a.B) * a.Hkv * rows) return;
   const int r = static_cast<int>(gr % rows);
   const int bk = static_cast<int>(gr / rows);
   const int kvh = bk % a.Hkv;
   const int b = bk / a.Hkv;
+  const int sg = (threadIdx.x % TPW) / TPR;
   const int d = (threadIdx.x % TPR) * 8;
   const int64_t rows_base =
       (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
   const float2* ml = a.ws_ml + rows_base * a.nsplit;
   const uint16_t* op = a.ws_o + rows_base * a.nsplit * D + d;
-  // the first min(nsplit, 8) slots are loaded before the prefix length is
-  // known (slots past this sequence's splits are in the workspace and their
-  // values are never used), so both round trips overlap
-  float2 mls[kMaxFast];
-  u16x8_t vs[kMaxFast];
+  // the first slots are loaded before the prefix length is known (slots
+  // past this sequence's splits are in the workspace and their values are
+  // never used), so both round trips overlap
+  float2 mls[kFast];
+  u16x8_t vs[kFast];
 #pragma unroll
-  for (int s = 0; s < kMaxFast; ++s) {
+  for (int i = 0; i < kFast; ++i) {
+    const int s = sg + SG * i;
     if (s < a.nsplit) {
-      mls[s] = ml[s];
-      vs[s] = *reinterpret_cast<const u16x8_t*>(op + static_cast<int64_t>(s) * D);
+      mls[i] = ml[s];
+      vs[i] = *reinterpret_cast<const u16x8_t*>(op + static_cast<int64_t>(s) * D);
     }
   }
   int c;
-  if (!seq_ok(a, b, c)) return;
+  if (!seq_ok(a, b, c)) return;                    // uniform over the row
   const int nsplit_b = seq_split(c, a.nsplit).n;
   float M = kNegInf;
 #pragma unroll
-  for (int s = 0; s < kMaxFast; ++s)
-    if (s < nsplit_b) M = fmaxf(M, mls[s].x);
-  for (int s = kMaxFast; s < nsplit_b; ++s) M = fmaxf(M, ml[s].x);
+  for (int i = 0; i < kFast; ++i)
+    if (sg + SG * i < nsplit_b) M = fmaxf(M, mls[i].x);
+  for (int s = sg + SG * kFast; s < nsplit_b; s += SG) M = fmaxf(M, ml[s].x);
+#pragma unroll
+  for (int off = TPR; off < TPW; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
   const float Mu = (M == kNegInf) ? 0.f : M;
   float L = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int s = 0; s < kMaxFast; ++s) {
-    if (s < nsplit_b) {
-      const float w = __builtin_amdgcn_exp2f(mls[s].x - Mu) * mls[s].y;
+  for (int i = 0; i < kFast; ++i) {
+    if (sg + SG * i < nsplit_b) {
+      const float w = __builtin_amdgcn_exp2f(mls[i].x - Mu) * mls[i].y;
       L += w;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) acc[k] += w * bf16_to_f32(vs[s][k]);
+      for (int k = 0; k < 8; ++k) acc[k] += w * bf16_to_f32(vs[i][k]);
     }
   }
-  for (int s = kMaxFast; s < nsplit_b; ++s) {
+  for (int s = sg + SG * kFast; s < nsplit_b; s += SG) {
     const float w = __builtin_amdgcn_exp2f(ml[s].x - Mu) * ml[s].y;
     L += w;
     const u16x8_t v = *reinterpret_cast<const u16x8_t*>(op + static_cast<int64_t>(s) * D);
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[k] += w * bf16_to_f32(v[k]);
   }
+#pragma unroll
+  for (int off = TPR; off < TPW; off <<= 1) {
+    L += __shfl_xor(L, off);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] += __shfl_xor(acc[k], off);
+  }
+  if (sg != 0) return;
   const int qi = r / a.G;
   const int qh = kvh * a.G + r % a.G;
   const int64_t t = static_cast<int64_t>(b) * a.W + qi;
@@ -964,6 +984,29 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
       a.packed ? a.out + packed_off(t, qh * D + d, a.Hq * D)
                : a.out + orow * D + d) = o8;
   if (a.lse && d == 0) a.lse[orow] = (M + __log2f(L)) * kLn2;
+}
+
+// Slot groups of the combine: enough that each thread loads at most eight
+// splits at once, at most one wave per row.
+template <int D, int SG>
+void launch_combine(const AttnArgs& a, hipStream_t st) {
+  const int64_t total_rows = static_cast<int64_t>(a.B) * a.Hkv * a.W * a.G;
+  constexpr int rpw = kCombineThreads / (D / 8 * SG);
+  hipLaunchKernelGGL((attn_combine_kernel<D, SG>),
+                     dim3(static_cast<unsigned>((total_rows + rpw - 1) / rpw)),
+                     dim3(kCombineThreads), 0, st, a);
+}
+
+template <int D>
+void combine(const AttnArgs& a, hipStream_t st) {
+  constexpr int kMaxSG = kWave / (D / 8);
+  const int sg = a.nsplit <= 8 ? 1 : a.nsplit <= 16 ? 2 : a.nsplit <= 32 ? 4 : 8;
+  switch (sg < kMaxSG ? sg : kMaxSG) {
+    case 1: launch_combine<D, 1>(a, st); break;
+    case 2: launch_combine<D, 2>(a, st); break;
+    case 4: launch_combine<D, 4>(a, st); break;
+    default: launch_combine<D, kMaxSG>(a, st); break;
+  }
 }
 
 template <int D>
@@ -993,11 +1036,7 @@ int launch(const AttnArgs& a, const Plan& p, hipStream_t st) {
   }
   WEDLM_LAUNCH_CHECK();
   if (a.nsplit > 1) {
-    const int64_t total_rows = static_cast<int64_t>(a.B) * a.Hkv * a.W * a.G;
-    constexpr int rpw = kCombineThreads / (D / 8);
-    hipLaunchKernelGGL((attn_combine_kernel<D>),
-                       dim3(static_cast<unsigned>((total_rows + rpw - 1) / rpw)),
-                       dim3(kCombineThreads), 0, st, a);
+    combine<D>(a, st);
     WEDLM_LAUNCH_CHECK();
   }
   return WEDLM_OK;

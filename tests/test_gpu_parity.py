@@ -226,6 +226,28 @@ def test_prefix_bound_far_above_the_prefixes():
     PL.check_commit(wl, d, g, o)
 
 
+@pytest.mark.parametrize("D,Hq,Hkv,W,prefix,lo", [
+    (128, 32, 8, 32, 3000, 2000),   # 11 split slots: two slot groups
+    (128, 16, 4, 32, 9000, 6000),   # 22 slots: four slot groups
+    (128, 8, 2, 32, 9000, 300),     # 35 slots: four groups of up to nine
+    (64, 2, 1, 16, 9000, 300),      # 35 slots: eight slot groups
+])
+def test_combine_slot_groups(D, Hq, Hkv, W, prefix, lo):
+    """Prefixes split more than eight ways: the combine spreads a row's
+    split slots over 2, 4 or 8 groups of lanes of one wave, each loading
+    its slots at once, and joins their max and sums by lane exchanges.
+    Sequences of one call use different numbers of splits."""
+    wl = WL.Workload("slots", 77 + D + prefix, B=3, W=W, Hq=Hq, Hkv=Hkv, D=D,
+                     V=400, prefix=prefix, prefix_hi=prefix, obs_frac=0.0,
+                     obs_frac_hi=0.75, spike=9.0, spike_prob=0.5)
+    d = WL.step_inputs(wl, seed=0)
+    # the block tables and caches cover prefix + W positions; the shorter
+    # prefixes use a part
+    d["win_start"][1:] = [lo, (lo + prefix) // 2 + 5]
+    _full_check(wl, d, [0, 1, 2], lambda b, n: _sample_rows(b, n, wl.W),
+                lambda b: sorted({0, Hq - 1, (5 * b) % Hq}))
+
+
 def test_prefix_beyond_one_split_of_pages():
     """A prefix longer than one split's staged page ids (2048 pages, 32,768
     positions) on a grid that already fills the CUs (16 sequences x 16 kv
