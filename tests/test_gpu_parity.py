@@ -368,11 +368,12 @@ def test_attention_workspace_reuse():
 
 def test_attention_workspace_shared_by_shapes():
     """One workspace, filled with random bytes first, serves calls of two
-    shapes in turn (their split plans place the arrival words and partials
-    at different offsets, so each call's words sit on bytes the other shape
-    wrote), three times over; every output is checked against the oracle.
-    The splits of a query block count their arrivals in those words and the
-    last one merges; bytes left by another call must never count."""
+    shapes in turn (their split plans place the partials and the (m, l)
+    pairs at different offsets, so each call's slots sit on bytes the other
+    shape wrote), three times over; every output is checked against the
+    oracle.  The combine reads only the slots of the splits a sequence
+    uses, which that call's main kernel has written; bytes left by another
+    call or shape must never enter a result."""
     import torch
     from oracle import wedlm_oracle as O
     from paper_2512_22737_amd import wedlm
