@@ -10,11 +10,16 @@
 // (for the memory stream the window is its own block, all filled, so the
 // result is plain causal attention).  The forward therefore lays the memory
 // stream's keys and values out as 16-position pages (the cache layout of
-// wedlm.h) and runs the window-attention kernel once over all 2K blocks of
-// every sequence, each block table row listing its sequence's pages in
-// order.  The prefix of each block is read from the pages in HBM/L2; no
-// block-sparse mask is materialised.
+// wedlm.h) and runs the window-attention kernel over the blocks, each block
+// table row listing its sequence's pages in order.  Memory block k and
+// prediction block k see the same prefix, so with 2B <= WEDLM_MAX_WINDOW
+// they run as one window of 2B rows (the kernel's paired mode: each half
+// sees the prefix and, causally, only its own block), and every prefix
+// tile staged in LDS serves both; larger blocks run one window each.  The
+// prefix is read from the pages in HBM/L2; no block-sparse mask is
+// materialised.
 #include "common.h"
+#include "internal.h"
 #include "wedlm_train.h"
 
 using namespace wedlm;
@@ -47,14 +52,14 @@ __global__ __launch_bounds__(256) void memory_pages_kernel(
   for (int e = 0; e < 8; ++e) dst[e * kPage] = vv[e];
 }
 
-// block s = (sequence, stream, block k): prefix k*B; block table row: the
-// sequence's L/16 pages in order
+// entry s = (sequence, stream, block k), or with paired blocks (sequence,
+// block k): prefix k*B; block table row: the sequence's L/16 pages in order
 __global__ __launch_bounds__(256) void block_meta_kernel(
-    int n_blocks, int K, int B, int P, int32_t* __restrict__ prefix,
-    int32_t* __restrict__ bt) {
+    int n_blocks, int K, int B, int P, int streams,
+    int32_t* __restrict__ prefix, int32_t* __restrict__ bt) {
   const int s = blockIdx.x;
-  const int sq = s / (2 * K);
-  const int kb = (s % (2 * K)) % K;
+  const int sq = s / (streams * K);
+  const int kb = (s % (streams * K)) % K;
   if (threadIdx.x == 0) prefix[s] = kb * B;
   for (int j = threadIdx.x; j < P; j += 256)
     bt[static_cast<int64_t>(s) * P + j] = sq * P + j;
@@ -62,6 +67,7 @@ __global__ __launch_bounds__(256) void block_meta_kernel(
 
 struct DsPlan {
   int K, P, n_blocks, max_prefix;
+  bool paired;            // memory and prediction block k in one window
   size_t kc, vc, prefix, bt, attn, total;
 };
 
@@ -77,7 +83,9 @@ bool ds_plan(int n_seq, int L, int B, int Hq, int Hkv, int D, DsPlan* p) {
     return false;
   p->K = L / B;
   p->P = L / kPage;
-  p->n_blocks = static_cast<int>(blocks);
+  p->paired = 2 * B <= WEDLM_MAX_WINDOW;
+  // block-table rows: one per pair, or one per block
+  p->n_blocks = static_cast<int>(p->paired ? blocks / 2 : blocks);
   p->max_prefix = (p->K - 1) * B;
   const size_t kv = static_cast<size_t>(n_seq) * L * Hkv * D * 2;
   size_t off = 0;
@@ -86,8 +94,11 @@ bool ds_plan(int n_seq, int L, int B, int Hq, int Hkv, int D, DsPlan* p) {
   p->prefix = off; off += up256(static_cast<size_t>(p->n_blocks) * 4);
   p->bt = off; off += up256(static_cast<size_t>(p->n_blocks) * p->P * 4);
   p->attn = off;
-  off += up256(wedlm_window_attn_workspace_size(p->n_blocks, B, Hq, Hkv, D,
-                                                p->max_prefix));
+  off += up256(p->paired
+                   ? window_attn_pairs_workspace_size(n_seq, p->K, B, Hq, Hkv,
+                                                      D, p->max_prefix)
+                   : wedlm_window_attn_workspace_size(p->n_blocks, B, Hq, Hkv,
+                                                      D, p->max_prefix));
   p->total = off;
   return true;
 }
@@ -128,8 +139,15 @@ extern "C" int wedlm_dual_stream_attn(const uint16_t* q, const uint16_t* k,
                      0, st, k, v, L, Hkv, D, items, kc, vc);
   WEDLM_LAUNCH_CHECK();
   hipLaunchKernelGGL(block_meta_kernel, dim3(p.n_blocks), dim3(256), 0, st,
-                     p.n_blocks, p.K, block, p.P, prefix, bt);
+                     p.n_blocks, p.K, block, p.P, p.paired ? 1 : 2, prefix,
+                     bt);
   WEDLM_LAUNCH_CHECK();
+  if (p.paired)
+    return window_attn_pairs(q, k, v, kc, vc,
+                             static_cast<int64_t>(n_seq) * p.P, bt, p.P,
+                             prefix, n_seq, p.K, block, Hq, Hkv, D,
+                             p.max_prefix, softmax_scale, out, lse,
+                             ws + p.attn, p.total - p.attn, stream);
   // the blocks in physical order are [n_seq][stream][K] windows of B rows:
   // q, k, v and out viewed as [n_blocks, B, heads, D]
   return wedlm_window_attn(q, k, v, kc, vc,

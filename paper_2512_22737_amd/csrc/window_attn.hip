@@ -72,6 +72,15 @@ struct AttnArgs {
   int B, W, Hq, Hkv, G, max_pages, max_prefix, nsplit, qblocks,
       rows_pad;
   int packed;             // out as the B*W x Hq*D matrix in packed MFMA tiles
+  // Paired blocks (pair_half = P > 0, W = 2P): "sequence" b is block
+  // b % pair_K of sequence b / pair_K of a [seq][2 streams][pair_K blocks]
+  // [P rows] layout; window rows 0..P-1 are the block of stream 0, rows
+  // P..2P-1 the block of stream 1, and a window key is visible only to the
+  // rows of its own half (causally).
+  int pair_half, pair_K;
+  // Workgroups take the sequences from the last one down (callers whose
+  // later sequences have the longer prefixes: the longest start first)
+  int rev;
   float scale_log2;       // softmax_scale * log2(e)
 };
 
@@ -154,6 +163,16 @@ __device__ __forceinline__ SeqSplit seq_split(int c, int nsplit) {
   r.len = per * kTileKeys;
   r.n = c > 0 ? (c + r.len - 1) / r.len : 1;
   return r;
+}
+
+// Physical row of window row qi of sequence b: b*W + qi, or with paired
+// blocks the row of that block and stream.
+__device__ __forceinline__ int64_t win_row(const AttnArgs& a, int b, int qi) {
+  if (a.pair_half == 0) return static_cast<int64_t>(b) * a.W + qi;
+  const int sq = b / a.pair_K, k = b - sq * a.pair_K;
+  const int half = qi >= a.pair_half ? 1 : 0;
+  return ((static_cast<int64_t>(sq) * 2 + half) * a.pair_K + k) * a.pair_half +
+         qi - half * a.pair_half;
 }
 
 // Sequence validity; bad lengths are reported and the sequence skipped.
@@ -291,7 +310,7 @@ void window_attn_kernel(AttnArgs a) {
   const int qb = wg % a.qblocks;
   wg /= a.qblocks;
   const int kvh = wg % a.Hkv;
-  const int b = wg / a.Hkv;
+  const int b = a.rev ? a.B - 1 - wg / a.Hkv : wg / a.Hkv;
 
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
@@ -311,8 +330,7 @@ void window_attn_kernel(AttnArgs a) {
     rvalid[q] = r < rows;
     qi[q] = rvalid[q] ? r / a.G : 0;
     qh[q] = kvh * a.G + (rvalid[q] ? r % a.G : 0);
-    const uint16_t* qp =
-        a.q + ((static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]) * D;
+    const uint16_t* qp = a.q + (win_row(a, b, qi[q]) * a.Hq + qh[q]) * D;
     // padded rows (past W*G) read row 0's query; their outputs are dropped
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk)
@@ -505,10 +523,14 @@ void window_attn_kernel(AttnArgs a) {
     for (int q = 0; q < QB; ++q) {
       if (need_mask) {
         const int lim = is_win ? min(a.W - 1, qi[q]) : lim_pre;
+        // paired blocks: a row of the second half sees no window key of
+        // the first
+        const int lo = is_win && a.pair_half > 0 && qi[q] >= a.pair_half
+                           ? a.pair_half : 0;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = base + 16 * (e >> 3) + 8 * hf + (e & 7);
-          sc[q][e] = key <= lim ? sc[q][e] : kNegInf;
+          sc[q][e] = key <= lim && key >= lo ? sc[q][e] : kNegInf;
         }
       }
       const float mx = col_max(sc[q]) * c2;
@@ -685,8 +707,7 @@ void window_attn_kernel(AttnArgs a) {
         if (base + key < a.W)
           v = *reinterpret_cast<const u16x8_t*>(
               (isv ? a.vw : a.kw) +
-              ((static_cast<int64_t>(b) * a.W + base + key) * a.Hkv + kvh) * D +
-              cc * 8);
+              (win_row(a, b, base + key) * a.Hkv + kvh) * D + cc * 8);
         r[u] = v;
       }
     }
@@ -851,7 +872,7 @@ tiles_done:
         (static_cast<int64_t>(b) * a.Hkv + kvh) * a.rows_pad + r;
     if (a.nsplit == 1) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      const int64_t t = static_cast<int64_t>(b) * a.W + qi[q];
+      const int64_t t = win_row(a, b, qi[q]);
       uint16_t* op = a.out + (t * a.Hq + qh[q]) * D;
 #pragma unroll
       for (int m = 0; m < NM; ++m)
@@ -867,8 +888,7 @@ tiles_done:
                        : op + d) = v;
         }
       if (a.lse && hf == 0)
-        a.lse[(static_cast<int64_t>(b) * a.W + qi[q]) * a.Hq + qh[q]] =
-            (m2[q] + __log2f(l_tot)) * kLn2;
+        a.lse[t * a.Hq + qh[q]] = (m2[q] + __log2f(l_tot)) * kLn2;
     } else {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
       uint16_t* wp = a.ws_o + (rows_base * a.nsplit + split) * D;
@@ -974,7 +994,7 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
   if (sg != 0) return;
   const int qi = r / a.G;
   const int qh = kvh * a.G + r % a.G;
-  const int64_t t = static_cast<int64_t>(b) * a.W + qi;
+  const int64_t t = win_row(a, b, qi);
   const int64_t orow = t * a.Hq + qh;
   const float inv = L > 0.f ? 1.f / L : 0.f;
   u16x8_t o8;
@@ -1077,9 +1097,12 @@ int window_attn_impl(
     int32_t B, int32_t W, int32_t Hq, int32_t Hkv, int32_t D,
     int32_t max_prefix_len, float softmax_scale, uint16_t* out, float* lse,
     int32_t* status, const Plan& p, void* workspace, hipStream_t st,
-    bool packed = false) {
+    bool packed = false, int pair_half = 0, int pair_K = 0, bool rev = false) {
   AttnArgs a{};
   a.packed = packed ? 1 : 0;
+  a.pair_half = pair_half;
+  a.pair_K = pair_K;
+  a.rev = rev ? 1 : 0;
   a.q = q_phys; a.kw = k_phys; a.vw = v_phys; a.kc = k_cache; a.vc = v_cache;
   a.bt = block_table; a.plen = prefix_len; a.out = out; a.lse = lse;
   a.status = status;
@@ -1207,4 +1230,49 @@ int wedlm::window_attn_packed(
                           Hq, Hkv, D, max_prefix_len, softmax_scale,
                           out_packed, nullptr, status, p, workspace,
                           static_cast<hipStream_t>(stream), true);
+}
+
+// The attention of paired blocks (Sec. 4.2's memory block k and prediction
+// block k share the prefix of the k*P memory positions before them): one
+// window of 2P rows per pair over that prefix, the two halves masked apart.
+// The prefix grows with the block index, so the workgroups take the pairs
+// from the last down: the longest run first and the short ones fill the
+// end of the grid.
+int wedlm::window_attn_pairs(
+    const uint16_t* q, const uint16_t* k, const uint16_t* v,
+    const uint16_t* k_cache, const uint16_t* v_cache, int64_t num_pages,
+    const int32_t* block_table, int32_t max_pages, const int32_t* prefix_len,
+    int32_t n_seq, int32_t blocks, int32_t P, int32_t Hq, int32_t Hkv,
+    int32_t D, int32_t max_prefix_len, float softmax_scale, uint16_t* out,
+    float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  if (n_seq < 1 || blocks < 1 || P < 1 || 2 * P > WEDLM_MAX_WINDOW)
+    return WEDLM_E_SHAPE;
+  const int64_t pairs = static_cast<int64_t>(n_seq) * blocks;
+  if (pairs > (1 << 30)) return WEDLM_E_SHAPE;
+  const int B = static_cast<int>(pairs), W = 2 * P;
+  const int e = check_args(q, k, v, k_cache, v_cache, num_pages, block_table,
+                           max_pages, prefix_len, B, W, Hq, Hkv, D,
+                           max_prefix_len, softmax_scale, out);
+  if (e != WEDLM_OK) return e;
+  const Plan p = make_plan(B, W, Hq, Hkv, D, max_prefix_len);
+  if (workspace_bytes < p.ws_bytes || (p.ws_bytes && !workspace))
+    return WEDLM_E_WORKSPACE;
+  return window_attn_impl(q, k, v, k_cache, v_cache, num_pages, block_table,
+                          max_pages, prefix_len, B, W, Hq, Hkv, D,
+                          max_prefix_len, softmax_scale, out, lse, nullptr, p,
+                          workspace, static_cast<hipStream_t>(stream), false,
+                          P, blocks, true);
+}
+
+size_t wedlm::window_attn_pairs_workspace_size(int32_t n_seq, int32_t blocks,
+                                               int32_t P, int32_t Hq,
+                                               int32_t Hkv, int32_t D,
+                                               int32_t max_prefix_len) {
+  if (n_seq < 1 || blocks < 1 || P < 1 || 2 * P > WEDLM_MAX_WINDOW) return 0;
+  const int64_t pairs = static_cast<int64_t>(n_seq) * blocks;
+  if (pairs > (1 << 30)) return 0;
+  if (!shape_ok(static_cast<int>(pairs), 2 * P, Hq, Hkv, D, max_prefix_len))
+    return 0;
+  return make_plan(static_cast<int>(pairs), 2 * P, Hq, Hkv, D, max_prefix_len)
+      .ws_bytes;
 }

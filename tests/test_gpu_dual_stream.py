@@ -1,8 +1,9 @@
 """GPU parity of wedlm_dual_stream_attn (include/wedlm_train.h) against the
 oracle's dense block mask (Sec. 4.2), within the attention bar of the
 decode step (max-abs 2e-2 and 1e-2 relative to the output scale; lse within
-1e-3): one and two sequences, blocks of 16 and 32, the decode step's head
-shapes and the Qwen3-8B heads."""
+1e-3): one and two sequences, blocks of 8, 16, 32 (paired windows) and 64
+(one window per block), the decode step's head shapes, the Qwen3-8B heads,
+and 8 query heads per kv head (two query blocks per paired window)."""
 import math
 
 import numpy as np
@@ -24,9 +25,13 @@ def _dev(a):
             .cuda().view(torch.bfloat16))
 
 
+# blocks of up to 32 run paired (memory block k and prediction block k in one
+# window of 2B rows, each half masked from the other's block); 64 one block
+# per window
 @pytest.mark.parametrize("n_seq,L,B,Hq,Hkv,D", [
     (1, 64, 16, 4, 2, 64), (2, 128, 32, 8, 2, 128), (1, 256, 32, 32, 8, 128),
-    (1, 96, 32, 4, 4, 64)])
+    (1, 96, 32, 4, 4, 64), (2, 64, 8, 8, 2, 64), (1, 192, 64, 8, 2, 128),
+    (1, 128, 32, 16, 2, 64)])
 def test_dual_stream_attention(n_seq, L, B, Hq, Hkv, D):
     from paper_2512_22737_amd import wedlm
     rng = np.random.default_rng(L + B + Hq)
