@@ -3,7 +3,9 @@ oracle's dense block mask (Sec. 4.2), within the attention bar of the
 decode step (max-abs 2e-2 and 1e-2 relative to the output scale; lse within
 1e-3): one and two sequences, blocks of 8, 16, 32 (paired windows) and 64
 (one window per block), the decode step's head shapes, the Qwen3-8B heads,
-and 8 query heads per kv head (two query blocks per paired window)."""
+8 query heads per kv head (two query blocks per paired window), and 32
+pairs of one kv head whose prefixes split three ways (the combine kernel in
+the paired layout)."""
 import math
 
 import numpy as np
@@ -31,7 +33,7 @@ def _dev(a):
 @pytest.mark.parametrize("n_seq,L,B,Hq,Hkv,D", [
     (1, 64, 16, 4, 2, 64), (2, 128, 32, 8, 2, 128), (1, 256, 32, 32, 8, 128),
     (1, 96, 32, 4, 4, 64), (2, 64, 8, 8, 2, 64), (1, 192, 64, 8, 2, 128),
-    (1, 128, 32, 16, 2, 64)])
+    (1, 128, 32, 16, 2, 64), (1, 1024, 32, 4, 1, 64)])
 def test_dual_stream_attention(n_seq, L, B, Hq, Hkv, D):
     from paper_2512_22737_amd import wedlm
     rng = np.random.default_rng(L + B + Hq)
