@@ -27,29 +27,47 @@ using namespace wedlm;
 namespace {
 
 // memory stream [n_seq, 2L, Hkv, D] rows 0..L-1 -> pages: K [P, Hkv, 16, D],
-// V [P, Hkv, D, 16] (P = n_seq * L / 16); one thread moves 8 values
+// V [P, Hkv, D, 16] (P = n_seq * L / 16).  One thread owns 8 consecutive d
+// of one head over the 16 positions of a page: it copies those K rows
+// (16-byte pieces, neighbouring lanes on neighbouring d) and transposes the
+// V rows in registers, so each of its 8 V^T rows is written as 32
+// contiguous bytes.
 __global__ __launch_bounds__(256) void memory_pages_kernel(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, int L,
     int Hkv, int D, int64_t n_items, uint16_t* __restrict__ kc,
     uint16_t* __restrict__ vc) {
+  static_assert(kPage == 16, "two 8-position halves per page");
   const int64_t it = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (it >= n_items) return;
   const int DG = D / 8;
   const int dg = static_cast<int>(it % DG);
   const int h = static_cast<int>((it / DG) % Hkv);
-  const int64_t sp = it / (DG * Hkv);               // sequence * L + position
-  const int64_t sq = sp / L;
-  const int p = static_cast<int>(sp % L);
-  const int64_t src = ((sq * 2 * L + p) * Hkv + h) * D + dg * 8;
-  const int64_t pg = sq * (L / kPage) + p / kPage;
-  const int row = p % kPage;
-  *reinterpret_cast<u16x8_t*>(kc + ((pg * Hkv + h) * kPage + row) * D +
-                              dg * 8) =
-      *reinterpret_cast<const u16x8_t*>(k + src);
-  const u16x8_t vv = *reinterpret_cast<const u16x8_t*>(v + src);
-  uint16_t* dst = vc + ((pg * Hkv + h) * D + dg * 8) * kPage + row;
+  const int64_t spg = it / (DG * Hkv);              // sequence * L/16 + page
+  const int64_t sq = spg / (L / kPage);
+  const int pp = static_cast<int>(spg % (L / kPage));
+  const int64_t src0 = ((sq * 2 * L + pp * kPage) * Hkv + h) * D + dg * 8;
+  const int64_t rstride = static_cast<int64_t>(Hkv) * D;   // one position
+  const int64_t pg = sq * (L / kPage) + pp;
+  u16x8_t vv[kPage];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) dst[e * kPage] = vv[e];
+  for (int r = 0; r < kPage; ++r)
+    vv[r] = *reinterpret_cast<const u16x8_t*>(v + src0 + r * rstride);
+#pragma unroll
+  for (int r = 0; r < kPage; ++r)
+    *reinterpret_cast<u16x8_t*>(kc + ((pg * Hkv + h) * kPage + r) * D + dg * 8) =
+        *reinterpret_cast<const u16x8_t*>(k + src0 + r * rstride);
+  uint16_t* dst = vc + ((pg * Hkv + h) * D + dg * 8) * kPage;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    u16x8_t lo, hi;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      lo[r] = vv[r][e];
+      hi[r] = vv[r + 8][e];
+    }
+    *reinterpret_cast<u16x8_t*>(dst + e * kPage) = lo;
+    *reinterpret_cast<u16x8_t*>(dst + e * kPage + 8) = hi;
+  }
 }
 
 // entry s = (sequence, stream, block k), or with paired blocks (sequence,
@@ -134,7 +152,7 @@ extern "C" int wedlm_dual_stream_attn(const uint16_t* q, const uint16_t* k,
   uint16_t* vc = reinterpret_cast<uint16_t*>(ws + p.vc);
   int32_t* prefix = reinterpret_cast<int32_t*>(ws + p.prefix);
   int32_t* bt = reinterpret_cast<int32_t*>(ws + p.bt);
-  const int64_t items = static_cast<int64_t>(n_seq) * L * Hkv * (D / 8);
+  const int64_t items = static_cast<int64_t>(n_seq) * (L / kPage) * Hkv * (D / 8);
   hipLaunchKernelGGL(memory_pages_kernel, dim3((items + 255) / 256), dim3(256),
                      0, st, k, v, L, Hkv, D, items, kc, vc);
   WEDLM_LAUNCH_CHECK();
