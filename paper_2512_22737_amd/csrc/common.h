@@ -42,6 +42,52 @@ __device__ __forceinline__ uint64_t ballot(bool p) {
 // Lane index within the wave.
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Word 3 of a raw buffer resource on gfx950 (32-bit data format, no
+// swizzle); reads past num_records return zero.
+constexpr int kBufferFlags = 0x00020000;
+
+// Raw buffer resource (stride 0) over num_bytes at base.
+__device__ __forceinline__ i32x4_t buffer_rsrc(const void* base,
+                                               int num_bytes) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  i32x4_t r;
+  r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(p & 0xffffffffu));
+  r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>((p >> 32) & 0xffffu));
+  r[2] = num_bytes;
+  r[3] = kBufferFlags;
+  return r;
+}
+
+// 16 bytes per lane from a raw buffer straight into LDS: lane l's data
+// lands at LDS byte lds_addr + 16*l (lds_addr is passed in M0).  Issued
+// through inline asm so the compiler does not guard every later LDS read
+// with a wait for these loads (it cannot tell which slot they write); the
+// kernel waits for them explicitly (wait_vmcnt) before the barrier that
+// publishes a slot.  NT: the non-temporal hint (a stream read once).
+template <bool NT = true>
+__device__ __forceinline__ void load_to_lds16(i32x4_t rsrc, int voff,
+                                              uint32_t lds_addr) {
+  if constexpr (NT)
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen nt lds"
+                 :
+                 : "v"(voff), "s"(rsrc), "{m0}"(lds_addr));
+  else
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voff), "s"(rsrc), "{m0}"(lds_addr));
+}
+
+// s_waitcnt with only the vector-memory counter bounded by N.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (((N >> 4) & 3) << 14) | (7 << 4) |
+                             (0xF << 8));
+}
+
 // Element (t, k) of an activation matrix with K columns (a multiple of 64)
 // in the packed MFMA tile layout of the projections: tile (t/32, k/64) at
 // 2048 * (t/32 * K/64 + k/64), then MFMA j = k%32 / 8 (512 elements each),

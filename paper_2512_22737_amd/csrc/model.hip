@@ -546,20 +546,22 @@ __global__ __launch_bounds__(256) void add_partials_kernel(
 // 2-D tiled GEMM for many window rows (M >= 128: batches of windows).  A
 // workgroup computes 256 features (8 blocks; for SwiGLU 4 gate blocks and
 // their 4 up blocks) x 128 tokens (4 row tiles) over its run of K steps.
-// Per 64-wide step the 12 packed 4 KB tiles (8 weight, 4 activation) are
-// copied to LDS as they are (the packed layout is already the MFMA operand
-// order, so the copy is 16 bytes per thread per chunk and every fragment
-// read is 16 contiguous bytes per lane); each of the 8 waves computes a
-// 64 x 64 piece (2 feature blocks x 2 row tiles, 16 MFMAs per step), so
-// every LDS byte a wave reads feeds two MFMAs.  Two register stages and two
-// LDS buffers: the tiles of step s+2 are loaded while step s computes, one
-// barrier per step.  Activations must be packed (ceil(M/32) tiles).
+// Per 64-wide step the 12 packed 4 KB tiles (8 weight, 4 activation) go
+// from HBM into LDS as they are, with LDS-destination buffer loads (the
+// packed layout is already the MFMA operand order, so every fragment read
+// is 16 contiguous bytes per lane and no register holds a tile in
+// transit); each of the 8 waves computes a 64 x 64 piece (2 feature blocks
+// x 2 row tiles, 16 MFMAs per step), so every LDS byte a wave reads feeds
+// two MFMAs.  A ring of three LDS stages: the tiles of step s+2 load while
+// step s computes, one barrier per step.  Activations must be packed
+// (ceil(M/32) tiles).
 // ---------------------------------------------------------------------------
 constexpr int k2dFeat = 8;                        // feature blocks per WG
 constexpr int k2dTok = 4;                         // row tiles per WG
 constexpr int k2dTiles = k2dFeat + k2dTok;        // 12 tiles per step
 constexpr int k2dStage = k2dTiles * kTile * 2;    // 48 KB per LDS buffer
-constexpr int k2dChunks = k2dTiles * 256 / kGThreads;   // 16 B per thread: 6
+constexpr int k2dChunks = k2dTiles * 4 / kGWaves;       // 1 KB chunks per wave: 6
+constexpr int k2dStages = 3;                      // LDS ring: 144 KB
 
 struct Gemm2dArgs {
   const uint16_t* x;      // packed activations, ceil(M/32) row tiles
@@ -573,7 +575,7 @@ struct Gemm2dArgs {
 
 template <int EPI>
 __global__ __launch_bounds__(kGThreads) void gemm2d_kernel(Gemm2dArgs a) {
-  __shared__ __attribute__((aligned(16))) char lds2[2 * k2dStage];
+  __shared__ __attribute__((aligned(1024))) char lds2[k2dStages * k2dStage];
   // tile order: the K splits and row tiles of one feature tile on one XCD
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
   const int per_ft = a.n_tt * a.n_ks;
@@ -598,30 +600,32 @@ __global__ __launch_bounds__(kGThreads) void gemm2d_kernel(Gemm2dArgs a) {
     const int fc = min(f, a.n_fb - 1);
     return (EPI == kSwiglu && i >= 4) ? fc + a.n_fb : fc;
   };
-  // this thread's 6 chunks of a step: LDS offset = chunk * 16 bytes
-  const uint16_t* src[k2dChunks];
+  // The 48 KB of a step go straight from HBM into its LDS stage: wave w
+  // moves the 1 KB chunks c = 6w .. 6w+5 (tile c / 4, MFMA j = c % 4), one
+  // load instruction each, lane l's 16 bytes landing at byte 16 l of the
+  // chunk, which is where the packed layout already keeps them.  Each chunk
+  // is read through a buffer resource over its tile's run of steps.
+  const uint32_t lds0 =
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds2));
+  i32x4_t rs[k2dChunks];
 #pragma unroll
-  for (int c = 0; c < k2dChunks; ++c) {
-    const int chunk = threadIdx.x + c * kGThreads;
-    const int tile = chunk >> 8, within = chunk & 255;
+  for (int u = 0; u < k2dChunks; ++u) {
+    const int tile = (wave * k2dChunks + u) >> 2;
     const int64_t blk = tile < k2dFeat ? wblock(tile)
                                        : min(tt * k2dTok + tile - k2dFeat, last_rt);
-    src[c] = (tile < k2dFeat ? a.w : a.x) + (blk * S + s0) * kTile + within * 8;
+    rs[u] = buffer_rsrc((tile < k2dFeat ? a.w : a.x) + (blk * S + s0) * kTile,
+                        n * kTile * 2);
   }
-  u16x8_t ra[k2dChunks], rb[k2dChunks];
-  auto gload = [&](int q, u16x8_t (&r)[k2dChunks]) {
+  auto issue = [&](int q, int stage) {
     const int qq = min(q, n - 1);                    // past the run: re-read
 #pragma unroll
-    for (int c = 0; c < k2dChunks; ++c)
-      r[c] = *reinterpret_cast<const u16x8_t*>(src[c] + qq * kTile);
+    for (int u = 0; u < k2dChunks; ++u) {
+      const int c = wave * k2dChunks + u;
+      load_to_lds16<false>(
+          rs[u], qq * kTile * 2 + (c & 3) * 1024 + lane * 16,
+          __builtin_amdgcn_readfirstlane(lds0 + stage * k2dStage + c * 1024));
+    }
   };
-  auto lstore = [&](int buf, const u16x8_t (&r)[k2dChunks]) {
-#pragma unroll
-    for (int c = 0; c < k2dChunks; ++c)
-      *reinterpret_cast<u16x8_t*>(lds2 + buf * k2dStage +
-                                  (threadIdx.x + c * kGThreads) * 16) = r[c];
-  };
-
   // wave tile: feature blocks fb0, fb0+1 (SwiGLU: gate fw and up fw + 4) x
   // row tiles 2*tw, 2*tw+1 of the workgroup
   const int fw = wave & 3, tw = wave >> 2;
@@ -651,27 +655,21 @@ __global__ __launch_bounds__(kGThreads) void gemm2d_kernel(Gemm2dArgs a) {
     }
   };
 
-  // step q computes from LDS buffer q&1; the tiles of q+1 sit in a register
-  // stage (loaded during q-1) and go to the other buffer after q computes;
-  // the tiles of q+2 load meanwhile into the other register stage.  The
-  // barrier ending step q-1 separates the reads of a buffer from its next
-  // write.
-  gload(0, ra);
-  lstore(0, ra);
-  gload(1, ra);
+  // step q computes from stage q % 3 while the loads of step q+2 fill stage
+  // (q+2) % 3, read last in step q-1 (before the barrier that ended it);
+  // before the barrier that ends step q every wave waits for its loads of
+  // step q+1, leaving only those of q+2 in flight.
+  issue(0, 0);
+  issue(1, 1);
+  wait_vmcnt<k2dChunks>();
   __syncthreads();
-  int q = 0;
-  for (; q + 2 <= n; q += 2) {
-    gload(q + 2, rb);
-    compute(0);
-    lstore(1, ra);
-    __syncthreads();
-    gload(q + 3, ra);
-    compute(1);
-    lstore(0, rb);
+  for (int q = 0; q < n; ++q) {
+    issue(q + 2, (q + 2) % k2dStages);
+    compute(q % k2dStages);
+    wait_vmcnt<k2dChunks>();
     __syncthreads();
   }
-  if (q < n) compute(0);
+  wait_vmcnt<0>();   // surplus re-reads retire before the workgroup ends
 
   // epilogue from registers: lane l, element e = 4g + r is feature
   // 8g + 4(l/32) + r of its block and token l%32 of its row tile, so the 4

@@ -182,14 +182,8 @@ __device__ __forceinline__ bool seq_ok(const AttnArgs& a, int b, int& c) {
          static_cast<int64_t>(c) <= static_cast<int64_t>(a.max_pages) * kPage;
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 typedef __attribute__((address_space(4))) const int32_t const_i32_t;
-typedef int i32x4_t __attribute__((ext_vector_type(4)));
-
-// Word 3 of a raw buffer resource on gfx950 (32-bit data format, no
-// swizzle); reads past num_records return zero.
-constexpr int kBufferFlags = 0x00020000;
 
 // Values of x in this lane and in the lane 32 away (v_permlane32_swap).
 __device__ __forceinline__ void xor32_pair(float x, float& a, float& b) {
@@ -205,40 +199,6 @@ __device__ __forceinline__ void xor32_pair(float x, float& a, float& b) {
 __device__ __forceinline__ int load_uniform(const int32_t* p, int idx) {
   idx = __builtin_amdgcn_readfirstlane(idx);
   return ((const_i32_t*)p)[idx];
-}
-
-// 16 bytes per lane from a raw buffer straight into LDS: lane l's data
-// lands at LDS byte lds_addr + 16*l (lds_addr is passed in M0).  Issued
-// through inline asm so the compiler does not guard every later LDS read
-// with a wait for these loads (it cannot tell which slot they write); the
-// kernel waits for them explicitly (wait_vmcnt) before the barrier that
-// publishes a slot.  The cache stream is read once, so the loads carry the
-// non-temporal hint.
-__device__ __forceinline__ void load_to_lds16(i32x4_t rsrc, int voff,
-                                              uint32_t lds_addr) {
-  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen nt lds"
-               :
-               : "v"(voff), "s"(rsrc), "{m0}"(lds_addr));
-}
-
-// Raw buffer resource (stride 0) over num_bytes at base.
-__device__ __forceinline__ i32x4_t buffer_rsrc(const void* base,
-                                               int num_bytes) {
-  const uint64_t p = reinterpret_cast<uint64_t>(base);
-  i32x4_t r;
-  r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(p & 0xffffffffu));
-  r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>((p >> 32) & 0xffffu));
-  r[2] = num_bytes;
-  r[3] = kBufferFlags;
-  return r;
-}
-
-// s_waitcnt with only the vector-memory counter bounded by N.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | (((N >> 4) & 3) << 14) | (7 << 4) |
-                             (0xF << 8));
 }
 
 // Layout of one 32-key tile in LDS (bytes).  The K halves of all slots
