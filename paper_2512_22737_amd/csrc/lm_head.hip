@@ -469,18 +469,25 @@ __global__ __launch_bounds__(kWave) void lm_head_merge_kernel(LmArgs a) {
 }
 
 // Row groups: up to 128 rows, one row wave with 1..4 blocks (a 256 x R
-// tile); up to 512 rows, groups of 256 rows in two row waves of 4 blocks (a
-// 128 x 256 tile: the same bytes per MFMA, half as many passes over the
-// weights; measured 29% faster at 384 rows); beyond, groups of 128 rows
-// again (measured faster at 1024 rows).  Narrower vocabulary tiles (more
-// row waves) re-stream the hidden rows from L2 faster than it delivers them.
+// tile); up to 512 rows, one or two groups in two row waves of 3 or 4
+// blocks each, the fewest blocks that cover R (a 128 x 192 or 128 x 256
+// tile: about the same bytes per MFMA as 256 x 128, half as many passes
+// over the weights; 256-row groups measured 29% faster than 128-row ones at
+// 384 rows, and 192-row groups leave no padded rows there); beyond, groups
+// of 128 rows again (measured faster at 1024 rows).  Narrower vocabulary
+// tiles (more row waves) re-stream the hidden rows from L2 faster than it
+// delivers them.
 struct Shape {
   int nb, rw;
 };
 
 Shape group_shape(int R) {
   if (R <= 128) return {(R + 31) / 32, 1};
-  if (R <= 512) return {4, 2};
+  if (R <= 512) {
+    const int groups = R <= 256 ? 1 : 2;
+    const int nb = (R + 64 * groups - 1) / (64 * groups);   // 3 or 4
+    return {nb < 3 ? 3 : nb, 2};
+  }
   return {4, 1};
 }
 
@@ -502,9 +509,9 @@ int resident_per_cu() {
   return n;
 }
 
-// the kernel of each group shape; occupancy index 0..4
-constexpr int kShapes = 5;
-int shape_index(Shape s) { return s.rw == 1 ? s.nb - 1 : 4; }
+// the kernel of each group shape; occupancy index 0..5
+constexpr int kShapes = 6;
+int shape_index(Shape s) { return s.rw == 1 ? s.nb - 1 : (s.nb == 3 ? 5 : 4); }
 
 // Slots per row group: every workgroup resident at once (CUs x occupancy),
 // no more streams than 32-row blocks.  Cached per device.
@@ -547,6 +554,7 @@ bool lm_plan(int R, int Hd, int V, LmPlan* p) {
     occ[dev][2] = resident_per_cu<3, 1, 2>();
     occ[dev][3] = resident_per_cu<4, 1, 2>();
     occ[dev][4] = resident_per_cu<4, 2, 2>();
+    occ[dev][5] = resident_per_cu<3, 2, 2>();
     occ_ks[dev][0] = ks_resident_per_cu<4>();
     occ_ks[dev][1] = ks_resident_per_cu<8>();
     cus[dev] = n;
@@ -640,6 +648,7 @@ extern "C" int wedlm_lm_head_score(const uint16_t* hidden,
       case 1: launch<2, 1, kPF>(nt, grid, st, a); break;
       case 2: launch<3, 1, 2>(nt, grid, st, a); break;
       case 3: launch<4, 1, 2>(nt, grid, st, a); break;
+      case 5: launch<3, 2, 2>(nt, grid, st, a); break;
       default: launch<4, 2, 2>(nt, grid, st, a); break;
     }
     WEDLM_LAUNCH_CHECK();

@@ -59,8 +59,10 @@ EXACT = [
     (40, 512, 513),      # two row blocks, ragged rows
     (96, 256, 2047),     # three row blocks
     (128, 512, 3001),    # four row blocks
+    (160, 512, 1500),    # one 192-row group in two row waves, ragged
     (200, 768, 1500),    # one 256-row group in two row waves
-    (300, 512, 2000),    # two 256-row groups, the second ragged
+    (300, 512, 2000),    # two 192-row groups, the second ragged
+    (448, 256, 1200),    # two 256-row groups, the second ragged
     (800, 256, 777),     # seven 128-row groups, the last ragged
     (17, 1024, 40000),   # several 32-row blocks per stream
     # k split over the waves (R <= 32, Hd 2048 / 4096)
