@@ -74,12 +74,11 @@ __global__ __launch_bounds__(256) void embed_kernel(
 // written back (the residual stream), then normalised.
 // A thread owns the float4 chunks c = tid + 256 i, i < CPT, of its row and
 // keeps them in registers: the loads of x, of the gain and of up to
-// kNormPre partials are all issued before the first add, so a row costs one
-// memory round trip before the reduction (CPT = 0: rows longer than 8192,
-// a loop over the chunks).
+// eight (or four) partials are all issued before the first add, so a row
+// costs one memory round trip before the reduction (CPT = 0: rows longer
+// than 8192, a loop over the chunks).
 // ---------------------------------------------------------------------------
 constexpr int kNormThreads = 256;
-constexpr int kNormPre = 4;
 
 template <bool ADD, bool XP, int CPT>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
@@ -110,6 +109,9 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
   };
 
   if constexpr (CPT > 0) {
+    // partials loaded before the first add: eight for rows of up to 4096,
+    // four for longer ones (registers)
+    constexpr int kNormPre = CPT <= 4 ? 8 : 4;
     floatx4_t v[CPT];
     u16x4_t gg[CPT];
 #pragma unroll
@@ -373,13 +375,16 @@ __device__ __forceinline__ void gemm_store(const GemmArgs& a, int tok, int n,
 // in the packed tile layout (ceil(M/32) tiles of 32 rows; rows past M are
 // never stored), so each activation load is 1 KB of contiguous memory too;
 // otherwise row-major, 64 contiguous bytes of a token row per lane and step.
-template <int NB, int NA, int PF, int EPI, bool NT, bool XP>
-__global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
+// NW: waves per workgroup (8, or 4 for the split residual-add products of
+// one 32-row block, whose K splits then run eight steps per wave).
+template <int NB, int NA, int PF, int EPI, bool NT, bool XP, int NW>
+__global__ __launch_bounds__(NW * kWave) void gemm_kernel(GemmArgs a) {
   constexpr int RB = 32 * NB;
   constexpr int TPC = 2;                            // tiles per LDS round
   constexpr int BPC = TPC / NA;                     // row blocks per round
   static_assert(NB % BPC == 0 || NB < BPC, "row blocks per round");
-  __shared__ float red[kGWaves * TPC * 32 * kRedStride];
+  static_assert(NW == 4 || NW == 8, "waves per workgroup");
+  __shared__ float red[NW * TPC * 32 * kRedStride];
 
   // the K splits and row groups of one feature block sit on one XCD (same
   // blockIdx % 8) at neighbouring positions: the row groups share its
@@ -398,8 +403,8 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
   const int col = lane & 31, hf = lane >> 5;
   const int S = a.K / kKStep;
   const int k0 = ks * S / a.n_ks, k1 = (ks + 1) * S / a.n_ks;
-  const int s0 = k0 + wave * (k1 - k0) / kGWaves;
-  const int s1 = k0 + (wave + 1) * (k1 - k0) / kGWaves;
+  const int s0 = k0 + wave * (k1 - k0) / NW;
+  const int s1 = k0 + (wave + 1) * (k1 - k0) / NW;
   const int n = s1 - s0;
 
   floatx16_t acc[NA][NB];
@@ -478,7 +483,7 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
       if (q + u < n) mfma(wa[u], xb[u]);
   }
 
-  // sum the 8 waves' partial tiles in wave order, TPC tiles per round
+  // sum the NW waves' partial tiles in wave order, TPC tiles per round
   constexpr int kRounds = (NA * NB + TPC - 1) / TPC;
 #pragma unroll
   for (int rd = 0; rd < kRounds; ++rd) {
@@ -496,11 +501,11 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
       }
     }
     __syncthreads();
-    // thread -> (feature f, token t): 32 features x 16 tokens, twice
+    // thread -> (feature f, token t): 32 features x 2 NW tokens per pass
     const int f = threadIdx.x & 31;
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const int tl = (threadIdx.x >> 5) + 16 * half;
+    for (int half = 0; half < 16 / NW; ++half) {
+      const int tl = (threadIdx.x >> 5) + 2 * NW * half;
 #pragma unroll
       for (int bb = 0; bb < BPC; ++bb) {
         const int tile0 = rd * TPC + bb * NA;
@@ -512,7 +517,7 @@ __global__ __launch_bounds__(kGThreads) void gemm_kernel(GemmArgs a) {
         for (int i = 0; i < NA; ++i) {
           float s = 0.f;
 #pragma unroll
-          for (int w = 0; w < kGWaves; ++w)
+          for (int w = 0; w < NW; ++w)
             s += red[((w * TPC + bb * NA + i) * 32 + f) * kRedStride + tl];
           v[i] = s;
         }
@@ -773,24 +778,24 @@ int gemm_nb(int M, bool swiglu) {
 
 // the largest row block of each kernel family also serves several row
 // groups; the smaller ones only ever run as one
-template <int NB, int NA, int PF, int EPI, bool XP>
+template <int NB, int NA, int PF, int EPI, bool XP, int NW = kGWaves>
 void gemm_launch_xp(const GemmArgs& a, hipStream_t st) {
   const int64_t grid = 8ll * a.n_rg * a.n_ks * ((a.n_nb + 7) / 8);
   if constexpr (NB * NA == 4) {
     if (a.n_rg > 1) {
-      hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, false, XP>), dim3(grid),
-                         dim3(kGThreads), 0, st, a);
+      hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, false, XP, NW>),
+                         dim3(grid), dim3(NW * kWave), 0, st, a);
       return;
     }
   }
-  hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, true, XP>), dim3(grid),
-                     dim3(kGThreads), 0, st, a);
+  hipLaunchKernelGGL((gemm_kernel<NB, NA, PF, EPI, true, XP, NW>), dim3(grid),
+                     dim3(NW * kWave), 0, st, a);
 }
 
-template <int NB, int NA, int PF, int EPI>
+template <int NB, int NA, int PF, int EPI, int NW = kGWaves>
 void gemm_launch(const GemmArgs& a, bool xp, hipStream_t st) {
-  if (xp) gemm_launch_xp<NB, NA, PF, EPI, true>(a, st);
-  else gemm_launch_xp<NB, NA, PF, EPI, false>(a, st);
+  if (xp) gemm_launch_xp<NB, NA, PF, EPI, true, NW>(a, st);
+  else gemm_launch_xp<NB, NA, PF, EPI, false, NW>(a, st);
 }
 
 bool gemm_shape_ok(int M, int N, int K) {
@@ -810,6 +815,7 @@ size_t up256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 // order.  No workgroup waits for another.
 struct GemmPlan {
   int nb, n_nb, n_rg, n_ks;
+  int nw;                 // waves per workgroup of the split-K kernel
   bool two_d;             // the 2-D tiled kernel (packed activations, many rows)
   int n_ft, n_tt;         // its feature and row tiles
   size_t part_bytes;
@@ -848,7 +854,16 @@ GemmPlan gemm_plan(int M, int N, int K, int epi, bool xp = false,
   p.n_nb = N / 32;
   p.n_rg = (M + 32 * p.nb - 1) / (32 * p.nb);
   p.n_ks = 1;
-  if (epi == kAddF32 || (epi == kStoreBf16 && split_store)) {
+  p.nw = kGWaves;
+  if (epi == kAddF32 && p.nb == 1 && K / kKStep <= 64) {
+    // one 32-row block and K up to 4096: four-wave workgroups, K split so
+    // that a wave runs about eight steps (at the o product's 4096 x 4096,
+    // 11.0 -> 9.6 us).  Longer K keeps eight waves and two splits: the down
+    // product split six ways this way took 24.1 against 23.0 us, and its
+    // RMSNorm then adds six partials
+    p.nw = 4;
+    p.n_ks = std::max(1, K / kKStep / (4 * 8));
+  } else if (epi == kAddF32 || (epi == kStoreBf16 && split_store)) {
     const int wgs = p.n_nb * p.n_rg;
     p.n_ks = std::max(1, std::min(kGemmTargetWgs / wgs, K / kKStep / kGWaves));
   }
@@ -917,7 +932,8 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
     if (nb == 1) gemm_launch<1, 2, 2, kSwiglu>(a, xp, st);
     else gemm_launch<2, 2, 2, kSwiglu>(a, xp, st);
   } else if (epi == kAddF32) {
-    if (nb == 1) gemm_launch<1, 1, 4, kAddF32>(a, xp, st);
+    if (nb == 1 && p.nw == 4) gemm_launch<1, 1, 4, kAddF32, 4>(a, xp, st);
+    else if (nb == 1) gemm_launch<1, 1, 4, kAddF32>(a, xp, st);
     else if (nb == 2) gemm_launch<2, 1, 2, kAddF32>(a, xp, st);
     else gemm_launch<4, 1, 2, kAddF32>(a, xp, st);
   } else {
