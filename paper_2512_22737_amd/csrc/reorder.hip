@@ -5,8 +5,9 @@
 // takes the i-th filled slot, row i >= n_obs the (i - n_obs)-th mask slot.
 // The row's angles are computed once in fp64 and shared through LDS; every
 // query and key head of the row is rotated in fp64 and rounded to bf16 (16
-// bytes per load and store), the value heads are copied.  The kernel moves (Hq + 2 Hkv) * D * 2 bytes in and
-// out per row; it is HBM-bound and small next to attention and scoring.
+// bytes per load and store), the value heads are copied.  The kernel moves
+// (Hq + 2 Hkv) * D * 2 bytes in and out per row; it is small next to
+// attention and scoring, and bound by the latency of its round trips.
 #include "common.h"
 
 using namespace wedlm;
@@ -56,18 +57,25 @@ __global__ __launch_bounds__(kThreads) void reorder_rope_kernel(
   const int H = Hq + 2 * Hkv;
   const uint16_t* x = qkv_in + (static_cast<int64_t>(b) * W + src) * H * D;
   // one item = 8 consecutive rotation pairs of one query or key head (two
-  // 16-byte loads, two 16-byte stores); the first round's loads go out
-  // before the angles are computed, so their latency hides under the fp64
-  // pow and sincos
+  // 16-byte loads, two 16-byte stores).  The first two rounds of items and
+  // the first round of the value copy are loaded before the angles are
+  // computed, so that one round trip covers a row of up to 512 items (the
+  // fp64 pow and sincos run under it)
   const int chunks = half / 8;                     // items per head
   const int n_items = (Hq + Hkv) * chunks;
-  int it = threadIdx.x;
-  u16x8_t lo8 = {}, hi8 = {};
-  if (it < n_items) {
-    const int head = it / chunks, j0 = (it - head * chunks) * 8;
-    lo8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0);
-    hi8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0 + half);
-  }
+  const int nv = Hkv * D / 8;                      // 16-byte pieces of v
+  auto load_item = [&](int it, u16x8_t& lo8, u16x8_t& hi8) {
+    if (it < n_items) {
+      const int head = it / chunks, j0 = (it - head * chunks) * 8;
+      lo8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0);
+      hi8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0 + half);
+    }
+  };
+  const u16x8_t* xv = reinterpret_cast<const u16x8_t*>(x + (Hq + Hkv) * D);
+  u16x8_t lo0 = {}, hi0 = {}, lo1 = {}, hi1 = {}, v0 = {};
+  load_item(threadIdx.x, lo0, hi0);
+  load_item(threadIdx.x + kThreads, lo1, hi1);
+  if (static_cast<int>(threadIdx.x) < nv) v0 = xv[threadIdx.x];
   if (threadIdx.x < half) {
     const int j = threadIdx.x;
     const double pos = static_cast<double>(win_start[b]) + src;
@@ -78,12 +86,9 @@ __global__ __launch_bounds__(kThreads) void reorder_rope_kernel(
     s_sin[j] = sn;
   }
   __syncthreads();
-  for (; it < n_items; it += kThreads) {
+  auto rotate = [&](int it, const u16x8_t& lo8, const u16x8_t& hi8) {
+    if (it >= n_items) return;
     const int head = it / chunks, j0 = (it - head * chunks) * 8;
-    if (it != static_cast<int>(threadIdx.x)) {
-      lo8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0);
-      hi8 = *reinterpret_cast<const u16x8_t*>(x + head * D + j0 + half);
-    }
     u16x8_t olo, ohi;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -100,12 +105,19 @@ __global__ __launch_bounds__(kThreads) void reorder_rope_kernel(
                   ((static_cast<int64_t>(b) * W + i) * Hkv + (head - Hq)) * D;
     *reinterpret_cast<u16x8_t*>(dst + j0) = olo;
     *reinterpret_cast<u16x8_t*>(dst + j0 + half) = ohi;
+  };
+  rotate(threadIdx.x, lo0, hi0);
+  rotate(threadIdx.x + kThreads, lo1, hi1);
+  for (int it = threadIdx.x + 2 * kThreads; it < n_items; it += kThreads) {
+    u16x8_t lo8 = {}, hi8 = {};
+    load_item(it, lo8, hi8);
+    rotate(it, lo8, hi8);
   }
-  // copy the value heads, 16 bytes per thread
-  const u16x8_t* xv = reinterpret_cast<const u16x8_t*>(x + (Hq + Hkv) * D);
+  // the value heads, 16 bytes per thread
   u16x8_t* dv = reinterpret_cast<u16x8_t*>(
       v_phys + (static_cast<int64_t>(b) * W + i) * Hkv * D);
-  for (int e = threadIdx.x; e < Hkv * D / 8; e += kThreads) dv[e] = xv[e];
+  if (static_cast<int>(threadIdx.x) < nv) dv[threadIdx.x] = v0;
+  for (int e = threadIdx.x + kThreads; e < nv; e += kThreads) dv[e] = xv[e];
 }
 
 }  // namespace

@@ -62,6 +62,9 @@ SMALL = [
     # blocks per kv head at D = 64 (384 rows)
     ("w64_d64_g4", 64, 8, 2, 64, (100, 900), (0.1, 0.6), 1500),
     ("w48_d64_g8", 48, 16, 2, 64, (40, 600), (0.0, 0.5), 640),
+    # 96 heads of 128: three rounds of rotation items per row in the
+    # reorder, two of value pieces
+    ("w8_d128_h96", 8, 64, 32, 128, (0, 100), (0.0, 0.8), 300),
 ]
 
 
