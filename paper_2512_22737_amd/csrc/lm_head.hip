@@ -76,20 +76,22 @@ __device__ __forceinline__ int h_off(int r, int c) {
   return r * (kKStep * 2) + ((c ^ (r & 7)) << 4);
 }
 
-// NB 32-row blocks of hidden rows per wave, RW row waves, HPF register
-// stages of hidden rows (a divisor of kPF); NT: weight loads carry the
+// NB 32-row blocks of hidden rows per wave, RW row waves, VB 32-row
+// vocabulary blocks per wave and step, HPF register stages of hidden rows
+// (a divisor of kPF); NT: weight loads carry the
 // non-temporal hint (one row group: nothing else reads the lines; with
 // several, the groups share them through L2 and the hint costs 5%)
-template <int NB, int RW, int HPF, bool NT>
+template <int NB, int RW, int HPF, bool NT, int VB = 1>
 __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   constexpr int VW = kWaves / RW;                   // vocabulary waves
   constexpr int RB = 32 * NB;                       // hidden rows per wave
   constexpr int RG = RB * RW;                       // hidden rows per group
-  constexpr int NJ = 4 / RW;                        // weight loads per wave
-  static_assert(kWaves % RW == 0 && 4 % RW == 0 && kPF % HPF == 0,
+  constexpr int BR = 32 * VB;                       // vocabulary rows per block
+  constexpr int NJ = 4 * VB / RW;                   // weight loads per wave
+  static_assert(kWaves % RW == 0 && (4 * VB) % RW == 0 && kPF % HPF == 0,
                 "wave and stage split");
   constexpr int kStage = RG * kKStep * 2;           // hidden LDS per step
-  constexpr int kWTile = 32 * kKStep * 2;           // weight LDS per step
+  constexpr int kWTile = BR * kKStep * 2;           // weight LDS per step
   constexpr int kWBase = 2 * kStage;                // weight tiles after
   constexpr int kRed = kWaves * RB * sizeof(State); // epilogue states
   constexpr int kMain = kWBase + VW * 2 * kWTile;
@@ -117,7 +119,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   const int nblk = a.nblk;
   const int total = nblk * nsteps;
 
-  // ---- weights: the stream's 32 rows x 128 bytes of a k step are four
+  // ---- weights: the stream's BR rows x 128 bytes of a k step are 4 VB
   // 1 KB loads (8 rows each, lane l: row l/8 + 8j, chunk l%8); row wave rw
   // issues loads j = rw, rw+RW, ...  Every load is issued (no branch in the
   // step, so the compiler's waits stay partial): a row past the stream's
@@ -125,7 +127,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   // end re-read the last.
   const int v_last = max(v_hi - 1, 0);
   const int w_row = lane >> 3, w_chunk = lane & 7;
-  char* const wtile = smem + kWBase + vw * 2 * kWTile;   // [2][32 x 128 B]
+  char* const wtile = smem + kWBase + vw * 2 * kWTile;   // [2][BR x 128 B]
   u16x8_t wa[kPF][NJ];
   auto wload = [&](int q, u16x8_t (&r)[NJ]) {
     q = min(q, total - 1);
@@ -134,7 +136,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
 #pragma unroll
     for (int i = 0; i < NJ; ++i) {
       const int rr = w_row + 8 * (rw + i * RW);
-      const int v = min(v_lo + 32 * bi + rr, v_last);
+      const int v = min(v_lo + BR * bi + rr, v_last);
       const u16x8_t* p = reinterpret_cast<const u16x8_t*>(
           a.w + static_cast<int64_t>(v) * a.Hd + s * kKStep + w_chunk * 8);
       if constexpr (NT)
@@ -182,12 +184,14 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   };
   auto hstep = [&](int s) { return ((s % nsteps) + nsteps) % nsteps; };
 
-  floatx16_t acc[NB];
+  floatx16_t acc[VB][NB];
   auto zero_acc = [&]() {
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+    for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[b][e] = 0.f;
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[vb][b][e] = 0.f;
   };
   zero_acc();
   State st[NB];
@@ -224,26 +228,37 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
       __attribute__((always_inline)) {
     const char* sb = smem + (u & 1) * kStage;
     const char* wb = wtile + (u & 1) * kWTile;
-    bf16x8_t afr[4];
+    // fragments of all four k slices read up front (one slice at a time
+    // with two vocabulary blocks per wave, for registers)
+    constexpr int KF = VB == 1 ? 4 : 1;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-      afr[kk] = __builtin_bit_cast(
-          bf16x8_t,
-          *reinterpret_cast<const u16x8_t*>(wb + h_off(col, hf * 4 + kk)));
-    bf16x8_t bfr[4][NB];
+    for (int k0 = 0; k0 < 4; k0 += KF) {
+      bf16x8_t afr[KF][VB];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
+      for (int kk = 0; kk < KF; ++kk)
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
-        bfr[kk][b] = __builtin_bit_cast(
-            bf16x8_t, *reinterpret_cast<const u16x8_t*>(
-                          sb + h_off(rw * RB + b * 32 + col, hf * 4 + kk)));
+        for (int vb = 0; vb < VB; ++vb)
+          afr[kk][vb] = __builtin_bit_cast(
+              bf16x8_t, *reinterpret_cast<const u16x8_t*>(
+                            wb + h_off(vb * 32 + col, hf * 4 + k0 + kk)));
+      bf16x8_t bfr[KF][NB];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
+      for (int kk = 0; kk < KF; ++kk)
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
-        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(afr[kk], bfr[kk][b],
-                                                         acc[b], 0, 0, 0);
+        for (int b = 0; b < NB; ++b)
+          bfr[kk][b] = __builtin_bit_cast(
+              bf16x8_t,
+              *reinterpret_cast<const u16x8_t*>(
+                  sb + h_off(rw * RB + b * 32 + col, hf * 4 + k0 + kk)));
+#pragma unroll
+      for (int kk = 0; kk < KF; ++kk) {
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            acc[vb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                afr[kk][vb], bfr[kk][b], acc[vb][b], 0, 0, 0);
+      }
     }
     wstore(wtile + ((u + 1) & 1) * kWTile, wa[(u + 1) % kPF]);
     wload(q + 1 + kPF, wa[(u + 1) % kPF]);
@@ -259,20 +274,23 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
         step(u, bi * nsteps + s0 + u, s0 + u);
     }
     // block done: lane (col, hf) of row block b holds logits of hidden row
-    // row0 + RB*rw + 32b + col at vocabulary rows v0 + 8*(e/4) + 4*hf + e%4
-    const int v0 = v_lo + 32 * bi;
+    // row0 + RB*rw + 32b + col at vocabulary rows
+    // v0 + 32*vb + 8*(e/4) + 4*hf + e%4
+    const int v0 = v_lo + BR * bi;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      float x[16];
-      int idx[16];
+    for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int v = v0 + 8 * (e >> 2) + 4 * hf + (e & 3);
-        idx[e] = v;
-        x[e] = v < v_hi ? acc[b][e] : kNegInf;
+      for (int b = 0; b < NB; ++b) {
+        float x[16];
+        int idx[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int v = v0 + 32 * vb + 8 * (e >> 2) + 4 * hf + (e & 3);
+          idx[e] = v;
+          x[e] = v < v_hi ? acc[vb][b][e] : kNegInf;
+        }
+        push_block(st[b], x, idx, sc);
       }
-      push_block(st[b], x, idx, sc);
-    }
     zero_acc();
   }
 
@@ -468,27 +486,28 @@ __global__ __launch_bounds__(kWave) void lm_head_merge_kernel(LmArgs a) {
   if (lane_id() == 0) finish(st, row, a.argmax, a.entropy, a.pmax);
 }
 
-// Row groups: up to 128 rows, one row wave with 1..4 blocks (a 256 x R
-// tile); up to 512 rows, one or two groups in two row waves of 3 or 4
-// blocks each, the fewest blocks that cover R (a 128 x 192 or 128 x 256
-// tile: about the same bytes per MFMA as 256 x 128, half as many passes
-// over the weights; 256-row groups measured 29% faster than 128-row ones at
-// 384 rows, and 192-row groups leave no padded rows there); beyond, groups
-// of 128 rows again (measured faster at 1024 rows).  Narrower vocabulary
-// tiles (more row waves) re-stream the hidden rows from L2 faster than it
-// delivers them.
+// Row groups: up to 96 rows, one row wave with 1..3 blocks (a 256 x R
+// tile); 97..128 rows, two row waves of 2 blocks; 129..256 rows, four row
+// waves of 2 blocks; 257..384 rows, four row waves of 3 blocks; beyond,
+// groups of 256 rows (four row waves of 2 blocks).  The multi-wave shapes
+// give each wave two 32-row vocabulary blocks, so a 64-row vocabulary
+// tile feeds every hidden-row fragment twice: the loop is bound by LDS
+// reads, and this takes them from 1.25 KB per MFMA (one vocabulary block,
+// four row blocks) to 1.0 (2 x 2) and 0.83 (2 x 3).  Measured against one
+// vocabulary block per wave: 9% faster at 128 and 1024 rows, 6% at 256,
+// 5% at 512, 17% at 384 (one group of 384 rows against two of 192).  Four
+// row blocks with two vocabulary blocks (128 accumulator registers) do not
+// fit in a wave's 256.
 struct Shape {
   int nb, rw;
+  int vb = 1;             // 32-row vocabulary blocks per wave and step
 };
 
 Shape group_shape(int R) {
-  if (R <= 128) return {(R + 31) / 32, 1};
-  if (R <= 512) {
-    const int groups = R <= 256 ? 1 : 2;
-    const int nb = (R + 64 * groups - 1) / (64 * groups);   // 3 or 4
-    return {nb < 3 ? 3 : nb, 2};
-  }
-  return {4, 1};
+  if (R <= 96) return {(R + 31) / 32, 1};
+  if (R <= 128) return {2, 2, 2};
+  if (R > 256 && R <= 384) return {3, 4, 2};
+  return {2, 4, 2};
 }
 
 // Hd a multiple of 4 k steps: the weight stages then line up with the steps
@@ -499,11 +518,12 @@ bool lm_shape_ok(int R, int Hd, int V) {
          static_cast<int64_t>(R) * Hd < (1ll << 31);
 }
 
-template <int NB, int RW, int HPF>
+template <int NB, int RW, int HPF, int VB = 1>
 int resident_per_cu() {
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &n, reinterpret_cast<const void*>(lm_head_kernel<NB, RW, HPF, true>),
+          &n,
+          reinterpret_cast<const void*>(lm_head_kernel<NB, RW, HPF, true, VB>),
           kThreads, 0) != hipSuccess || n < 1)
     n = 1;
   return n;
@@ -511,7 +531,10 @@ int resident_per_cu() {
 
 // the kernel of each group shape; occupancy index 0..5
 constexpr int kShapes = 6;
-int shape_index(Shape s) { return s.rw == 1 ? s.nb - 1 : (s.nb == 3 ? 5 : 4); }
+int shape_index(Shape s) {
+  if (s.vb == 1) return s.nb - 1;
+  return s.rw == 2 ? 3 : s.nb == 2 ? 4 : 5;
+}
 
 // Slots per row group: every workgroup resident at once (CUs x occupancy),
 // no more streams than 32-row blocks.  Cached per device.
@@ -552,9 +575,9 @@ bool lm_plan(int R, int Hd, int V, LmPlan* p) {
     occ[dev][0] = resident_per_cu<1, 1, kPF>();
     occ[dev][1] = resident_per_cu<2, 1, kPF>();
     occ[dev][2] = resident_per_cu<3, 1, 2>();
-    occ[dev][3] = resident_per_cu<4, 1, 2>();
-    occ[dev][4] = resident_per_cu<4, 2, 2>();
-    occ[dev][5] = resident_per_cu<3, 2, 2>();
+    occ[dev][3] = resident_per_cu<2, 2, 2, 2>();
+    occ[dev][4] = resident_per_cu<2, 4, 2, 2>();
+    occ[dev][5] = resident_per_cu<3, 4, 1, 2>();
     occ_ks[dev][0] = ks_resident_per_cu<4>();
     occ_ks[dev][1] = ks_resident_per_cu<8>();
     cus[dev] = n;
@@ -572,30 +595,32 @@ bool lm_plan(int R, int Hd, int V, LmPlan* p) {
   p->sh = group_shape(R);
   const int rg = 32 * p->sh.nb * p->sh.rw;
   const int vw = kWaves / p->sh.rw;
+  const int br = 32 * p->sh.vb;
   p->n_rg = (R + rg - 1) / rg;
   int n_slot = cus[dev] * occ[dev][shape_index(p->sh)] / p->n_rg;
-  const int by_blocks = (V + 32 * vw - 1) / (32 * vw);
+  const int by_blocks = (V + br * vw - 1) / (br * vw);
   if (n_slot > by_blocks) n_slot = by_blocks;
   if (n_slot < 1) n_slot = 1;
   p->n_slot = n_slot;
   const int64_t S = static_cast<int64_t>(n_slot) * vw;
   const int64_t per = (V + S - 1) / S;               // rows of the longest
-  p->nblk = static_cast<int>((per + 31) / 32);
+  p->nblk = static_cast<int>((per + br - 1) / br);
   return true;
 }
 
 // groups of fewer than 128 rows only occur with R < 128: one group
-template <int NB, int RW, int HPF>
+// only the 256-row shape ever serves several row groups (nt false)
+template <int NB, int RW, int HPF, int VB = 1>
 void launch(bool nt, int64_t grid, hipStream_t st, const LmArgs& a) {
-  if constexpr (NB * RW < 4) {
-    hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, true>), dim3(grid),
+  if constexpr (32 * NB * RW != 256) {
+    hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, true, VB>), dim3(grid),
                        dim3(kThreads), 0, st, a);
   } else {
     if (nt)
-      hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, true>), dim3(grid),
+      hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, true, VB>), dim3(grid),
                          dim3(kThreads), 0, st, a);
     else
-      hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, false>), dim3(grid),
+      hipLaunchKernelGGL((lm_head_kernel<NB, RW, HPF, false, VB>), dim3(grid),
                          dim3(kThreads), 0, st, a);
   }
 }
@@ -647,9 +672,9 @@ extern "C" int wedlm_lm_head_score(const uint16_t* hidden,
       case 0: launch<1, 1, kPF>(nt, grid, st, a); break;
       case 1: launch<2, 1, kPF>(nt, grid, st, a); break;
       case 2: launch<3, 1, 2>(nt, grid, st, a); break;
-      case 3: launch<4, 1, 2>(nt, grid, st, a); break;
-      case 5: launch<3, 2, 2>(nt, grid, st, a); break;
-      default: launch<4, 2, 2>(nt, grid, st, a); break;
+      case 3: launch<2, 2, 2, 2>(nt, grid, st, a); break;
+      case 4: launch<2, 4, 2, 2>(nt, grid, st, a); break;
+      default: launch<3, 4, 1, 2>(nt, grid, st, a); break;
     }
     WEDLM_LAUNCH_CHECK();
   }

@@ -58,12 +58,17 @@ EXACT = [
     (32, 256, 1000),     # one row block, ragged vocabulary ranges
     (40, 512, 513),      # two row blocks, ragged rows
     (96, 256, 2047),     # three row blocks
-    (128, 512, 3001),    # four row blocks
-    (160, 512, 1500),    # one 192-row group in two row waves, ragged
-    (200, 768, 1500),    # one 256-row group in two row waves
-    (300, 512, 2000),    # two 192-row groups, the second ragged
+    (97, 256, 1000),     # one 128-row group in two row waves of two blocks
+                         # (two vocabulary blocks per wave), 31 padded rows
+    (128, 512, 3001),    # one full 128-row group
+    (160, 512, 1500),    # one 256-row group in four row waves, ragged
+    (200, 768, 1500),    # one 256-row group, ragged
+    (300, 512, 2000),    # one 384-row group (four row waves, two vocabulary
+                         # blocks per wave), ragged rows
+    (384, 256, 1111),    # one full 384-row group, vocabulary ranges ending
+                         # inside a 64-row block
     (448, 256, 1200),    # two 256-row groups, the second ragged
-    (800, 256, 777),     # seven 128-row groups, the last ragged
+    (800, 256, 777),     # four 256-row groups, the last ragged
     (17, 1024, 40000),   # several 32-row blocks per stream
     # k split over the waves (R <= 32, Hd 2048 / 4096)
     (7, 2048, 33),       # two blocks, the second with one row
