@@ -15,23 +15,25 @@
 //               wave v is stream j = slot*VW + v of its row group, which owns
 //               the contiguous vocabulary range [j*V/S, (j+1)*V/S) (S = VW
 //               n_slot streams), so ranges differ by at most one row; it
-//               walks the range in 32-row blocks.  The RW row waves of a
+//               walks the range in blocks of 32*VB rows (VB = 1, or 2 for
+//               the shapes with several row waves).  The RW row waves of a
 //               stream take NB 32-row blocks of hidden rows each (a row
 //               group is 32*NB*RW rows), read the same weights (fetched once
 //               per CU, then from L1) and keep a running score state per row
-//               (RW is 2 for 129..512 rows, else 1)
 //   MFMA      = v_mfma_f32_32x32x16_bf16 computing logits^T: A = 32 weight
-//               rows x 16 k (registers), B = 16 k x 32 hidden rows (LDS)
+//               rows x 16 k, B = 16 k x 32 hidden rows, both read from LDS;
+//               a wave's step is VB x NB MFMAs per 16-wide k slice
 //   k order   = the contraction runs over k in a permuted order that is the
 //               same for A and B: in each 64-wide k step, lane half hf of
 //               MFMA j takes k = 32*hf + 8*j .. +8, i.e. 16-byte chunk
 //               4*hf + j of a 128-byte LDS row, for both operands.
 // Memory path: the weights are the HBM stream (V * Hd * 2 bytes per row
-//   group).  A stream's 32 rows of a k step (4 KB) are loaded coalesced,
-//   eight full 128-byte rows per wave instruction, split over its row waves,
-//   PF steps ahead across block boundaries, and go through a double-buffered
-//   LDS tile of the stream (a pattern with one row per lane touches 32 lines
-//   per instruction and streams about 25% slower).  The hidden rows of a
+//   group).  A stream's 32*VB rows of a k step (4 KB per 32 rows) are
+//   loaded coalesced, eight full 128-byte rows per wave instruction, split
+//   over its row waves, PF steps ahead across block boundaries, and go
+//   through a double-buffered LDS tile of the stream (a pattern with one
+//   row per lane touches 32 lines per instruction and streams about 25%
+//   slower).  The hidden rows of a
 //   step go through LDS the same way.  All LDS rows are XOR-swizzled 16-byte
 //   chunks; one barrier per step orders every buffer.
 //   Slots are placed so that the row groups of one slot share an XCD (and
@@ -119,7 +121,7 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   const int nblk = a.nblk;
   const int total = nblk * nsteps;
 
-  // ---- weights: the stream's BR rows x 128 bytes of a k step are 4 VB
+  // ---- weights: the stream's BR rows x 128 bytes of a k step are 4*VB
   // 1 KB loads (8 rows each, lane l: row l/8 + 8j, chunk l%8); row wave rw
   // issues loads j = rw, rw+RW, ...  Every load is issued (no branch in the
   // step, so the compiler's waits stay partial): a row past the stream's
