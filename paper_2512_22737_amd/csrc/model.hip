@@ -727,6 +727,133 @@ __global__ __launch_bounds__(kGThreads) void gemm2d_kernel(Gemm2dArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wide SwiGLU tiles for large grids: a workgroup computes 128 features
+// (gate blocks 0..3 and their up blocks) x 256 tokens (8 row tiles) over
+// the whole K.  Wave w takes gate block w%4 and its up block x row tiles
+// 4(w/4) .. 4(w/4)+3: each A fragment read from LDS feeds four MFMAs and
+// each B fragment two, 0.75 KB of LDS reads per MFMA against 1 KB in the
+// kernel above.  Per step the 16 packed tiles (64 KB) go to LDS as there;
+// a ring of two stages (128 KB): the tiles of step s+1 load while step s
+// computes.  Each output element sums its k steps in the same order as the
+// kernel above, so the two give the same bits.  Used when its grid fills
+// most of the chip (at 512 rows and 12288 features: 92-99 against 109-127
+// us); on smaller grids the 128-token tiles are faster.
+// ---------------------------------------------------------------------------
+constexpr int kWTok = 8;                          // row tiles per WG
+constexpr int kWTiles = k2dFeat + kWTok;          // 16 tiles per step
+constexpr int kWStage = kWTiles * kTile * 2;      // 64 KB per LDS buffer
+constexpr int kWChunks = kWTiles * 4 / kGWaves;   // 1 KB chunks per wave: 8
+constexpr int kWStages = 2;                       // LDS ring: 128 KB
+
+__global__ __launch_bounds__(kGThreads) void gemm2d_swiglu_wide_kernel(
+    Gemm2dArgs a) {
+  __shared__ __attribute__((aligned(1024))) char lds2[kWStages * kWStage];
+  // tile order: the row tiles of one feature tile on one XCD
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int ft = xcd + 8 * (local / a.n_tt);
+  const int tt = local % a.n_tt;
+  if (ft >= a.n_ft) return;                          // whole workgroup
+
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int n = a.K / kKStep;
+  const int last_rt = (a.M - 1) / 32;
+  // gate blocks 0..3 then their up blocks (clamped at the end: those
+  // outputs are never stored)
+  auto wblock = [&](int i) {
+    const int f = ft * (k2dFeat / 2) + (i & 3);
+    const int fc = min(f, a.n_fb - 1);
+    return i >= 4 ? fc + a.n_fb : fc;
+  };
+  // wave w moves the 1 KB chunks c = 8w .. 8w+7 (tile c / 4, MFMA c % 4)
+  const uint32_t lds0 =
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds2));
+  i32x4_t rs[kWChunks];
+#pragma unroll
+  for (int u = 0; u < kWChunks; ++u) {
+    const int tile = (wave * kWChunks + u) >> 2;
+    const int64_t blk = tile < k2dFeat
+                            ? wblock(tile)
+                            : min(tt * kWTok + tile - k2dFeat, last_rt);
+    rs[u] = buffer_rsrc((tile < k2dFeat ? a.w : a.x) + blk * n * kTile,
+                        n * kTile * 2);
+  }
+  auto issue = [&](int q, int stage) {
+    const int qq = min(q, n - 1);                    // past the run: re-read
+#pragma unroll
+    for (int u = 0; u < kWChunks; ++u) {
+      const int c = wave * kWChunks + u;
+      load_to_lds16<false>(
+          rs[u], qq * kTile * 2 + (c & 3) * 1024 + lane * 16,
+          __builtin_amdgcn_readfirstlane(lds0 + stage * kWStage + c * 1024));
+    }
+  };
+  const int fw = wave & 3, tw = wave >> 2;
+  floatx16_t acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  auto compute = [&](int buf) {
+    const char* base = lds2 + buf * kWStage + lane * 16;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bf16x8_t a0 =
+          *reinterpret_cast<const bf16x8_t*>(base + fw * 4096 + j * 1024);
+      const bf16x8_t a1 = *reinterpret_cast<const bf16x8_t*>(
+          base + (fw + 4) * 4096 + j * 1024);
+      bf16x8_t b[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        b[t] = *reinterpret_cast<const bf16x8_t*>(
+            base + (k2dFeat + 4 * tw + t) * 4096 + j * 1024);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        acc[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b[t], acc[0][t], 0, 0, 0);
+        acc[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b[t], acc[1][t], 0, 0, 0);
+      }
+    }
+  };
+
+  // step q computes from stage q % 2 while the loads of step q+1 fill the
+  // other stage, read last in step q-1 (before the barrier that ended it);
+  // before the barrier that ends step q every wave waits for its loads.
+  issue(0, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int q = 0; q < n; ++q) {
+    issue(q + 1, (q + 1) & 1);
+    compute(q & 1);
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+
+  // epilogue as in gemm2d_kernel (lane l, element 4g + r: feature
+  // 8g + 4(l/32) + r of its block, token l%32 of its row tile)
+  const int hf = lane >> 5, col = lane & 31;
+#pragma unroll
+  for (int tj = 0; tj < 4; ++tj) {
+    const int tok = (tt * kWTok + 4 * tw + tj) * 32 + col;
+    if (tok >= a.M) continue;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int f = (ft * (k2dFeat / 2) + fw) * 32 + 8 * g + 4 * hf;
+      if (f >= a.N) continue;
+      u16x4_t o;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float gg = acc[0][tj][4 * g + r], uu = acc[1][tj][4 * g + r];
+        o[r] = f32_to_bf16(gg / (1.0f + expf(-gg)) * uu);
+      }
+      *reinterpret_cast<u16x4_t*>(static_cast<uint16_t*>(a.out) +
+                                  packed_off(tok, f, a.N)) = o;
+    }
+  }
+}
+
 // out[t][n] (bf16) = sum over splits k (in order) of part[k][t][n], four
 // consecutive n per thread (N a multiple of 32, ldo of 4)
 __global__ __launch_bounds__(256) void sum_partials_bf16_kernel(
@@ -817,6 +944,7 @@ struct GemmPlan {
   int nb, n_nb, n_rg, n_ks;
   int nw;                 // waves per workgroup of the split-K kernel
   bool two_d;             // the 2-D tiled kernel (packed activations, many rows)
+  bool wide;              // its 256-token SwiGLU tiles
   int n_ft, n_tt;         // its feature and row tiles
   size_t part_bytes;
 };
@@ -829,6 +957,9 @@ constexpr int k2dMinRows = 256;
 // workgroups a split product aims at: about one per CU (with few rows, 512
 // and 768 made the 36-layer step at B = 1 slower: 5.00 -> 5.29 and 5.91 ms)
 constexpr int kGemmTargetWgs = 256;
+// the wide SwiGLU tiles from this many workgroups (three quarters of the
+// CUs; at 96 or 128 workgroups the 128-token tiles measured faster)
+constexpr int kWideMinWgs = 3 * kGemmTargetWgs / 4;
 
 GemmPlan gemm_plan(int M, int N, int K, int epi, bool xp = false,
                    bool split_store = false) {
@@ -841,6 +972,13 @@ GemmPlan gemm_plan(int M, int N, int K, int epi, bool xp = false,
     p.n_ft = (p.n_nb + (epi == kSwiglu ? 3 : 7)) / (epi == kSwiglu ? 4 : 8);
     p.n_tt = (M + 32 * k2dTok - 1) / (32 * k2dTok);
     p.n_ks = 1;
+    if (epi == kSwiglu) {
+      const int n_tt_w = (M + 32 * kWTok - 1) / (32 * kWTok);
+      if (p.n_ft * n_tt_w >= kWideMinWgs) {
+        p.wide = true;
+        p.n_tt = n_tt_w;
+      }
+    }
     // a stored product (q|k|v) with few tiles splits K too; its fp32
     // partials are summed into bf16 right after
     if (epi == kAddF32 || epi == kStoreBf16)
@@ -892,7 +1030,10 @@ int gemm(const uint16_t* x, const uint16_t* w, int M, int N, int K, void* out,
     g.n_fb = p.n_nb; g.n_ft = p.n_ft; g.n_tt = p.n_tt; g.n_ks = p.n_ks;
     const int64_t grid = 8ll * p.n_tt * p.n_ks * ((p.n_ft + 7) / 8);
     if (grid > (1ll << 30)) return WEDLM_E_SHAPE;
-    if (epi == kSwiglu)
+    if (p.wide)
+      hipLaunchKernelGGL(gemm2d_swiglu_wide_kernel, dim3(grid),
+                         dim3(kGThreads), 0, st, g);
+    else if (epi == kSwiglu)
       hipLaunchKernelGGL(gemm2d_kernel<kSwiglu>, dim3(grid), dim3(kGThreads),
                          0, st, g);
     else if (epi == kAddF32)

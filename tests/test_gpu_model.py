@@ -367,13 +367,13 @@ def test_decoder_graph_replay_matches_eager():
     assert torch.equal(v0.view(torch.int16), v1.view(torch.int16))
 
 
-@pytest.mark.parametrize("B", [2, 8])
+@pytest.mark.parametrize("B", [2, 8, 16])
 def test_qwen3_shaped_layer_against_oracle(B):
     """One layer at the Qwen3-8B sizes (hidden 4096, 32/8 heads of 128, MLP
     12288; vocabulary cut to 4096), B sequences of W = 32: 64 rows (the
-    split-K products, the RMSNorms summing split partials) or 256 rows (the
+    split-K products, the RMSNorms summing split partials), 256 rows (the
     2-D tiled products, o's input packed, residual-add products split over
-    8 workgroups).  Prefill of 64 prompt tokens, then two streaming steps
+    8 workgroups) or 512 rows (the gate/up product in 256-token tiles).  Prefill of 64 prompt tokens, then two streaming steps
     checked against the full-sequence oracle as in the tiny decoder test."""
     ms = WL.ModelShape("qwen3_8b_1l_v4k", 302, L=1, Hd=4096, Hq=32, Hkv=8,
                        D=128, I=12288, V=4096)
