@@ -33,9 +33,10 @@
 //   over its row waves, PF steps ahead across block boundaries, and go
 //   through a double-buffered LDS tile of the stream (a pattern with one
 //   row per lane touches 32 lines per instruction and streams about 25%
-//   slower).  The hidden rows of a
-//   step go through LDS the same way.  All LDS rows are XOR-swizzled 16-byte
-//   chunks; one barrier per step orders every buffer.
+//   slower).  The hidden rows of a step go through LDS the same way
+//   (groups beyond 384 rows load both straight into LDS instead:
+//   lm_head_dma_kernel).  All LDS rows are XOR-swizzled 16-byte chunks;
+//   one barrier per step orders every buffer.
 //   Slots are placed so that the row groups of one slot share an XCD (and
 //   the weights they stream in its L2).
 // Epilogue: after each block a lane holds 16 logits of one hidden row per
@@ -318,6 +319,177 @@ __global__ __launch_bounds__(kThreads) void lm_head_kernel(LmArgs a) {
   }
 }
 
+// Large row groups: the same decomposition, but a step's hidden rows and
+// weights go from memory straight into one of two LDS stages with
+// LDS-destination buffer loads (lane l of a 1 KB load lands at LDS row l/8,
+// slot l%8, so it fetches the chunk (l%8) ^ (l/8) that the XOR swizzle puts
+// there).  With no register staging a wave can hold 64 vocabulary x 128
+// hidden rows of accumulators (NB 4, RW 4, VB 2: a 512-row group, one pass
+// over the weights, 0.75 KB of LDS reads per MFMA).  The loads of step q+1
+// are issued before step q computes and waited for before the barrier that
+// ends it.  Weights are read through a buffer resource over the stream's
+// own rows, hidden rows through one over the group's rows (reads past them
+// return zero; rows past the range are clamped to its last one and their
+// logits masked), so every offset is that of a few megabytes.
+template <int NB, int RW, int VB, bool NT>
+__global__ __launch_bounds__(kThreads) void lm_head_dma_kernel(LmArgs a) {
+  constexpr int VW = kWaves / RW;
+  constexpr int RB = 32 * NB;
+  constexpr int RG = RB * RW;
+  constexpr int BR = 32 * VB;
+  constexpr int kHStage = RG * kKStep * 2;
+  constexpr int kWTileB = BR * kKStep * 2;
+  constexpr int kStageB = kHStage + VW * kWTileB;
+  constexpr int kHLoads = RG / 8 / kWaves;
+  constexpr int kWLoads = BR / 8 / RW;
+  static_assert(RG % (8 * kWaves) == 0 && BR % (8 * RW) == 0, "load split");
+  constexpr int kRed = kWaves * RB * sizeof(State);
+  constexpr int kLds = 2 * kStageB > kRed ? 2 * kStageB : kRed;
+  __shared__ __attribute__((aligned(1024))) char smem[kLds];
+
+  const int xcd = blockIdx.x % 8;
+  const int local = blockIdx.x / 8;
+  const int rg = local % a.n_rg;
+  const int slot = (local / a.n_rg) * 8 + xcd;
+  if (slot >= a.n_slot) return;
+
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int vw = wave % VW;
+  const int rw = wave / VW;
+  const int lane = lane_id();
+  const int col = lane & 31;
+  const int hf = lane >> 5;
+  const int row0 = rg * RG;
+  const int64_t S = static_cast<int64_t>(a.n_slot) * VW;
+  const int64_t j = static_cast<int64_t>(slot) * VW + vw;
+  const int v_lo = static_cast<int>(j * a.V / S);
+  const int v_hi = static_cast<int>((j + 1) * a.V / S);
+  const int nsteps = a.Hd / kKStep;
+  const int nblk = a.nblk;
+  const int total = nblk * nsteps;
+
+  const int lr = lane >> 3;
+  const int lc = (lane & 7) ^ lr;
+  const int w_rows = max(v_hi - v_lo, 1);
+  const i32x4_t wrs = buffer_rsrc(a.w + static_cast<int64_t>(v_lo) * a.Hd,
+                                  (v_hi - v_lo) * a.Hd * 2);
+  const int h_rows = min(a.R - row0, RG);
+  const i32x4_t hrs = buffer_rsrc(a.hidden + static_cast<int64_t>(row0) * a.Hd,
+                                  h_rows * a.Hd * 2);
+  const uint32_t lds0 =
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)smem));
+  auto issue = [&](int q, int stage) {
+    q = min(q, total - 1);
+    const int bi = q / nsteps;
+    const int s = q - bi * nsteps;
+#pragma unroll
+    for (int i = 0; i < kHLoads; ++i) {
+      const int blk = wave + kWaves * i;
+      const int r = min(8 * blk + lr, h_rows - 1);
+      load_to_lds16<false>(hrs, r * a.Hd * 2 + s * 128 + lc * 16,
+                           __builtin_amdgcn_readfirstlane(
+                               lds0 + stage * kStageB + blk * 1024));
+    }
+#pragma unroll
+    for (int i = 0; i < kWLoads; ++i) {
+      const int blk = rw + RW * i;
+      const int rr = min(BR * bi + 8 * blk + lr, w_rows - 1);
+      load_to_lds16<NT>(wrs, rr * a.Hd * 2 + s * 128 + lc * 16,
+                        __builtin_amdgcn_readfirstlane(
+                            lds0 + stage * kStageB + kHStage + vw * kWTileB +
+                            blk * 1024));
+    }
+  };
+
+  floatx16_t acc[VB][NB];
+  auto zero_acc = [&]() {
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[vb][b][e] = 0.f;
+  };
+  zero_acc();
+  State st[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) st[b] = empty_state();
+  const ExpScale sc = exp_scale(a.c2);
+
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const char* sb = smem + buf * kStageB;
+    const char* wb = sb + kHStage + vw * kWTileB;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      bf16x8_t afr[VB], bfr[NB];
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb)
+        afr[vb] = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u16x8_t*>(
+                          wb + h_off(vb * 32 + col, hf * 4 + kk)));
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        bfr[b] = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u16x8_t*>(
+                          sb + h_off(rw * RB + b * 32 + col, hf * 4 + kk)));
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          acc[vb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              afr[vb], bfr[b], acc[vb][b], 0, 0, 0);
+    }
+  };
+
+  issue(0, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int bi = 0; bi < nblk; ++bi) {
+    for (int s = 0; s < nsteps; ++s) {
+      const int q = bi * nsteps + s;
+      issue(q + 1, (q + 1) & 1);
+      compute(q & 1);
+      wait_vmcnt<0>();
+      __syncthreads();
+    }
+    const int v0 = v_lo + BR * bi;
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        float x[16];
+        int idx[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int v = v0 + 32 * vb + 8 * (e >> 2) + 4 * hf + (e & 3);
+          idx[e] = v;
+          x[e] = v < v_hi ? acc[vb][b][e] : kNegInf;
+        }
+        push_block(st[b], x, idx, sc);
+      }
+    zero_acc();
+  }
+
+  State* red = reinterpret_cast<State*>(smem);
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    merge(st[b], shfl_xor_state(st[b], 32), a.c2);
+    if (hf == 0) red[wave * RB + b * 32 + col] = st[b];
+  }
+  __syncthreads();
+  if (threadIdx.x < RG) {
+    const int r = threadIdx.x;
+    const int r_w = r / RB, r_l = r % RB;
+    State m = red[(r_w * VW) * RB + r_l];
+    for (int v = 1; v < VW; ++v) merge(m, red[(r_w * VW + v) * RB + r_l], a.c2);
+    const int row = row0 + r;
+    if (row < a.R) {
+      if (a.n_slot == 1) finish(m, row, a.argmax, a.entropy, a.pmax);
+      else a.ws[static_cast<int64_t>(row) * a.n_slot + slot] = m;
+    }
+  }
+}
+
 // Few rows (R <= 32): the k split over the waves.  A workgroup of NWV
 // waves owns a contiguous run of 32-row vocabulary blocks (the runs of the
 // grid differ by at most one block); wave w owns the k steps w, w + NWV,
@@ -491,25 +663,29 @@ __global__ __launch_bounds__(kWave) void lm_head_merge_kernel(LmArgs a) {
 // Row groups: up to 96 rows, one row wave with 1..3 blocks (a 256 x R
 // tile); 97..128 rows, two row waves of 2 blocks; 129..256 rows, four row
 // waves of 2 blocks; 257..384 rows, four row waves of 3 blocks; beyond,
-// groups of 256 rows (four row waves of 2 blocks).  The multi-wave shapes
-// give each wave two 32-row vocabulary blocks, so a 64-row vocabulary
-// tile feeds every hidden-row fragment twice: the loop is bound by LDS
-// reads, and this takes them from 1.25 KB per MFMA (one vocabulary block,
-// four row blocks) to 1.0 (2 x 2) and 0.83 (2 x 3).  Measured against one
-// vocabulary block per wave: 9% faster at 128 and 1024 rows, 6% at 256,
-// 5% at 512, 17% at 384 (one group of 384 rows against two of 192).  Four
-// row blocks with two vocabulary blocks (128 accumulator registers) do not
-// fit in a wave's 256.
+// groups of 512 rows in four row waves of 4 blocks (lm_head_dma_kernel).
+// The multi-wave shapes give each wave two 32-row vocabulary blocks, so a
+// 64-row vocabulary tile feeds every hidden-row fragment twice: the loop
+// is bound by LDS reads, and this takes them from 1.25 KB per MFMA (one
+// vocabulary block, four row blocks) to 1.0 (2 x 2), 0.83 (2 x 3) and
+// 0.75 (2 x 4).  Measured against one vocabulary block per wave: 9% faster
+// at 128 rows, 6% at 256, 17% at 384 (one group of 384 rows against two of
+// 192).  The 512-row groups need the register-free staging of the DMA
+// kernel (128 accumulator registers) and against 256-row groups measured
+// 14% faster at 448 and 512 rows, 39% at 768 and 12% at 1024; at 384 rows
+// the DMA kernel with 3 blocks ties the register-staged one.
 struct Shape {
   int nb, rw;
   int vb = 1;             // 32-row vocabulary blocks per wave and step
+  bool dma = false;       // lm_head_dma_kernel
 };
 
 Shape group_shape(int R) {
   if (R <= 96) return {(R + 31) / 32, 1};
   if (R <= 128) return {2, 2, 2};
-  if (R > 256 && R <= 384) return {3, 4, 2};
-  return {2, 4, 2};
+  if (R <= 256) return {2, 4, 2};
+  if (R <= 384) return {3, 4, 2};
+  return {4, 4, 2, true};
 }
 
 // Hd a multiple of 4 k steps: the weight stages then line up with the steps
@@ -532,8 +708,9 @@ int resident_per_cu() {
 }
 
 // the kernel of each group shape; occupancy index 0..5
-constexpr int kShapes = 6;
+constexpr int kShapes = 7;
 int shape_index(Shape s) {
+  if (s.dma) return 6;
   if (s.vb == 1) return s.nb - 1;
   return s.rw == 2 ? 3 : s.nb == 2 ? 4 : 5;
 }
@@ -564,6 +741,25 @@ int ks_resident_per_cu() {
   return n;
 }
 
+template <int NB, int RW, int VB>
+int dma_resident_per_cu() {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &n, reinterpret_cast<const void*>(lm_head_dma_kernel<NB, RW, VB, true>),
+          kThreads, 0) != hipSuccess || n < 1)
+    n = 1;
+  return n;
+}
+template <int NB, int RW, int VB>
+void launch_dma(bool nt, int64_t grid, hipStream_t st, const LmArgs& a) {
+  if (nt)
+    hipLaunchKernelGGL((lm_head_dma_kernel<NB, RW, VB, true>), dim3(grid),
+                       dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((lm_head_dma_kernel<NB, RW, VB, false>), dim3(grid),
+                       dim3(kThreads), 0, st, a);
+}
+
 bool lm_plan(int R, int Hd, int V, LmPlan* p) {
   if (!lm_shape_ok(R, Hd, V)) return false;
   int dev = 0;
@@ -580,6 +776,7 @@ bool lm_plan(int R, int Hd, int V, LmPlan* p) {
     occ[dev][3] = resident_per_cu<2, 2, 2, 2>();
     occ[dev][4] = resident_per_cu<2, 4, 2, 2>();
     occ[dev][5] = resident_per_cu<3, 4, 1, 2>();
+    occ[dev][6] = dma_resident_per_cu<4, 4, 2>();
     occ_ks[dev][0] = ks_resident_per_cu<4>();
     occ_ks[dev][1] = ks_resident_per_cu<8>();
     cus[dev] = n;
@@ -594,19 +791,29 @@ bool lm_plan(int R, int Hd, int V, LmPlan* p) {
     p->nblk = 0;
     return true;
   }
-  p->sh = group_shape(R);
-  const int rg = 32 * p->sh.nb * p->sh.rw;
-  const int vw = kWaves / p->sh.rw;
-  const int br = 32 * p->sh.vb;
-  p->n_rg = (R + rg - 1) / rg;
-  int n_slot = cus[dev] * occ[dev][shape_index(p->sh)] / p->n_rg;
-  const int by_blocks = (V + br * vw - 1) / (br * vw);
-  if (n_slot > by_blocks) n_slot = by_blocks;
-  if (n_slot < 1) n_slot = 1;
-  p->n_slot = n_slot;
-  const int64_t S = static_cast<int64_t>(n_slot) * vw;
-  const int64_t per = (V + S - 1) / S;               // rows of the longest
-  p->nblk = static_cast<int>((per + br - 1) / br);
+  auto slots = [&](Shape sh) {
+    p->sh = sh;
+    const int rg = 32 * sh.nb * sh.rw;
+    const int vw = kWaves / sh.rw;
+    const int br = 32 * sh.vb;
+    p->n_rg = (R + rg - 1) / rg;
+    int n_slot = cus[dev] * occ[dev][shape_index(sh)] / p->n_rg;
+    const int by_blocks = (V + br * vw - 1) / (br * vw);
+    if (n_slot > by_blocks) n_slot = by_blocks;
+    if (n_slot < 1) n_slot = 1;
+    p->n_slot = n_slot;
+    const int64_t S = static_cast<int64_t>(n_slot) * vw;
+    const int64_t per = (V + S - 1) / S;             // rows of the longest
+    p->nblk = static_cast<int>((per + br - 1) / br);
+    return per;
+  };
+  const Shape sh = group_shape(R);
+  const int64_t per = slots(sh);
+  // the DMA kernel's buffer resources hold 32-bit byte counts: a stream's
+  // weight rows and a group's hidden rows must stay under 2 GiB
+  if (sh.dma && (per * Hd * 2 >= (1ll << 31) ||
+                 static_cast<int64_t>(32 * sh.nb * sh.rw) * Hd * 2 >= (1ll << 31)))
+    slots(Shape{2, 4, 2});
   return true;
 }
 
@@ -676,7 +883,8 @@ extern "C" int wedlm_lm_head_score(const uint16_t* hidden,
       case 2: launch<3, 1, 2>(nt, grid, st, a); break;
       case 3: launch<2, 2, 2, 2>(nt, grid, st, a); break;
       case 4: launch<2, 4, 2, 2>(nt, grid, st, a); break;
-      default: launch<3, 4, 1, 2>(nt, grid, st, a); break;
+      case 5: launch<3, 4, 1, 2>(nt, grid, st, a); break;
+      default: launch_dma<4, 4, 2>(nt, grid, st, a); break;
     }
     WEDLM_LAUNCH_CHECK();
   }

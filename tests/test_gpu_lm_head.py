@@ -67,8 +67,10 @@ EXACT = [
                          # blocks per wave), ragged rows
     (384, 256, 1111),    # one full 384-row group, vocabulary ranges ending
                          # inside a 64-row block
-    (448, 256, 1200),    # two 256-row groups, the second ragged
-    (800, 256, 777),     # four 256-row groups, the last ragged
+    (448, 256, 1200),    # one 512-row group (LDS-destination loads), ragged
+    (512, 512, 3001),    # one full 512-row group
+    (513, 256, 999),     # two 512-row groups, the second of one row
+    (800, 256, 777),     # two 512-row groups, the second ragged
     (17, 1024, 40000),   # several 32-row blocks per stream
     # k split over the waves (R <= 32, Hd 2048 / 4096)
     (7, 2048, 33),       # two blocks, the second with one row
