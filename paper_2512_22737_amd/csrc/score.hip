@@ -11,15 +11,15 @@
 // two non-negative terms, so nothing cancels even when H is ~1e-25 (strongly
 // peaked rows at T = 0.1).
 //
-// Accuracy of e^z (score_state.h): the exponent y = (l - l_max) * log2(e)/T
-// is formed in fp32 from split constants, log2(e)/T = c2h + c2l and
-// l_max * c2h = mch + mcl (its exact fused-multiply-add residual), as
-// fma(l, c2h, -mch) - mcl + (l - l_max) * c2l; no rounding is shared by all
-// the terms of a row, and v_exp_f32 gives 2^y.  Only the rescaling of a
-// state to a new maximum evaluates its exponent in fp64.
+// Accuracy of e^z: the exponent y = (l - m) * log2(e)/T (m the wave's
+// running maximum) is formed in fp32 as fma(d, c2h, d * c2l) with
+// d = l - m (exact when l and m are close) and log2(e)/T = c2h + c2l split
+// into an fp32 head and tail, so no rounding is shared by all the terms of
+// a row; v_exp_f32 gives 2^y.  Only the rescaling of a state to a new
+// maximum evaluates its exponent in fp64.
 //
 // Roofline: 4*V bytes per masked row, read once.
-// Work: with 768 rows or more, one workgroup per row (observed rows exit)
+// Work: with 512 rows or more, one workgroup per row (observed rows exit)
 // and no partials.  With fewer rows the chunking follows the rows that are
 // masked in this call, known only on the device: every workgroup counts
 // them (Mt, from n_obs), splits each into nch = ceil(768 / Mt) vocabulary
@@ -330,10 +330,16 @@ __global__ __launch_bounds__(kWave) void score_merge_kernel(ScoreArgs a) {
   if (lane_id() == 0) finish(st, b * a.W + i, a.argmax, a.entropy, a.pmax);
 }
 
+// Window rows from which every row takes one workgroup, unchunked: at 512
+// rows (384 masked at long_prefix, about 222 in the streaming loop) the
+// merge kernel's launch cost more than the chunks gained (score 45.5
+// against 48.8 us at long_prefix, the loop's step 0.137 against 0.138 ms).
+constexpr int kWholeRows = 512;
+
 // Chunks per row at most (0: no chunking, one workgroup per row): with
-// fewer than 768 rows and a vocabulary of more than one 16K chunk.
+// fewer than kWholeRows rows and a vocabulary of more than one 16K chunk.
 int plan_max_nchunk(int B, int W, int V) {
-  if (static_cast<int64_t>(B) * W >= kTargetWgs) return 0;
+  if (static_cast<int64_t>(B) * W >= kWholeRows) return 0;
   const int n = (V + kMinChunk - 1) / kMinChunk;
   return n > 1 ? n : 0;
 }

@@ -45,7 +45,8 @@ def _logits(rng, B, W, V, stride):
     (1, 32, 151936, 151936, [31]),                # one masked row
     (2, 8, 40000, 40000, [8, 8]),                 # none masked
     (300, 1, 40001, 40004, None),                 # 300 sequences, W = 1
-    (16, 32, 20001, 20003, None),                 # two chunks at most, unaligned rows
+    (16, 32, 20001, 20003, None),                 # 512 rows: one workgroup each, unaligned rows
+    (73, 7, 20001, 20001, None),                  # 511 rows: chunked, two chunks at most
     (3, 16, 5000, 5000, [-4, 20, 7]),             # one chunk per row; n_obs clamped
     (800, 1, 3000, 3000, None),                   # 800 rows: one workgroup each
 ])
