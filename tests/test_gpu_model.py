@@ -367,17 +367,20 @@ def test_decoder_graph_replay_matches_eager():
     assert torch.equal(v0.view(torch.int16), v1.view(torch.int16))
 
 
-@pytest.mark.parametrize("B", [2, 8, 16])
-def test_qwen3_shaped_layer_against_oracle(B):
+@pytest.mark.parametrize("B,W", [(2, 32), (8, 32), (16, 32), (13, 31)])
+def test_qwen3_shaped_layer_against_oracle(B, W):
     """One layer at the Qwen3-8B sizes (hidden 4096, 32/8 heads of 128, MLP
-    12288; vocabulary cut to 4096), B sequences of W = 32: 64 rows (the
+    12288; vocabulary cut to 4096), B sequences of W slots: 64 rows (the
     split-K products, the RMSNorms summing split partials), 256 rows (the
     2-D tiled products, o's input packed, residual-add products split over
-    8 workgroups) or 512 rows (the gate/up product in 256-token tiles).  Prefill of 64 prompt tokens, then two streaming steps
-    checked against the full-sequence oracle as in the tiny decoder test."""
+    8 workgroups), 512 rows (the gate/up product in 256-token tiles) or 403
+    rows (those tiles with a partly filled last row tile and a partly used
+    second group of 256 tokens).  Prefill of 2W prompt tokens, then two
+    streaming steps checked against the full-sequence oracle as in the tiny
+    decoder test."""
     ms = WL.ModelShape("qwen3_8b_1l_v4k", 302, L=1, Hd=4096, Hq=32, Hkv=8,
                        D=128, I=12288, V=4096)
-    W, c0, T = 32, 64, 1.0
+    c0, T = 2 * W, 1.0                  # prompt of two all-filled windows
     wbits = WL.model_weights(ms, seed=0)
     wf = MO.decode(wbits)
     dec, bt = _decoder(ms, wbits, B, W, pages_per_seq=10, T=T)
